@@ -1,0 +1,358 @@
+"""Benchmark of the quantized conv2d + requantize path on one MI355X.
+
+Default workload: the ResNet-50 conv stack at batch 32 (stem, 16 bottlenecks,
+4 projection shortcuts: 53 conv2d + bias + requantize (+ReLU) layers, NHWC
+uint8 activations with random zero points, per-channel int8 weights), seeded
+synthetic data.  A step runs every layer once on its own resident input;
+the step is captured once into a HIP graph and replayed.
+
+Printed (stdout, one JSON line): effective int8 TOP/s = 2 * algorithmic MACs
+of the step / step time (MACs = N*Ho*Wo*Cout*R*S*Cin, zero-point corrections,
+padding of the GEMM shape and the epilogue not counted), the roofline of the
+dominant kernel, and the CPU oracle timed on a bounded sample.
+
+Other workloads (--workload): mobilenet_v2_b64, inception_v3_b64, dense_bert,
+conv14x14x64 -- the same measurement on those layer sets (depthwise layers
+and adds are reported in GB/s in the per-layer file).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_INT8_TOPS = 5000.0   # MI355X dense int8 MFMA, TOP/s
+PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, GB/s
+METRIC = "effective int8 TOPS + % of int8 MFMA peak, qnn.conv2d+requantize"
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ workloads
+
+def _layers(name):
+    import workloads as W
+    if name == "resnet50_b32":
+        return [("conv", l, W.conv_case(l, 32, seed=3000 + i)) for i, l in enumerate(W.resnet50())], 32
+    if name == "resnet50_b1":
+        return [("conv", l, W.conv_case(l, 1, seed=3000 + i)) for i, l in enumerate(W.resnet50())], 1
+    if name == "mobilenet_v2_b64":
+        out = []
+        for i, l in enumerate(W.mobilenet_v2_layers()):
+            if isinstance(l, W.AddLayer):
+                out.append(("add", l, W.add_case(l, 64, seed=4000 + i)))
+            else:
+                out.append(("dw" if l.depthwise else "conv", l, W.conv_case(l, 64, seed=4000 + i)))
+        return out, 64
+    if name == "inception_v3_b64":
+        return [("conv", l, W.conv_case(l, 64, seed=5000 + i)) for i, l in enumerate(W.inception_v3())], 64
+    if name == "dense_bert":
+        return [("dense", l, W.dense_case(l, seed=2 + i)) for i, l in enumerate(W.bert_ffn())], 128
+    if name == "conv14x14x64":
+        c = W.single_conv_case()
+        return [("conv", W.SINGLE_CONV, c)], 1
+    raise SystemExit(f"unknown workload {name}")
+
+
+def _macs(kind, layer, case, out_shape):
+    if kind == "dense":
+        return layer.M * layer.K * layer.N
+    if kind == "add":
+        return 0
+    N, Ho, Wo, K = out_shape
+    if kind == "dw":
+        return N * Ho * Wo * K * layer.R * layer.S
+    return N * Ho * Wo * K * layer.R * layer.S * layer.Cin
+
+
+def _bytes(kind, layer, case, out_shape):
+    """Algorithmic HBM bytes: every input byte once, weights once, every
+    output byte once."""
+    if kind == "add":
+        return case.a.nbytes * 3
+    out = int(np.prod(out_shape))
+    return case.x.nbytes + case.w.nbytes + out
+
+
+class Item:
+    pass
+
+
+def setup(workload):
+    import torch
+    from paper_2006_10226_amd import qnn as Q
+
+    layers, batch = _layers(workload)
+    items = []
+    for kind, layer, c in layers:
+        it = Item()
+        it.kind, it.layer, it.name = kind, layer, layer.name
+        if kind == "add":
+            it.a = torch.from_numpy(c.a).cuda()
+            it.b = torch.from_numpy(c.b).cuda()
+            it.out = torch.empty_like(it.a)
+            it.case = c
+            it.desc = "add"
+            it.macs, it.bytes = 0, _bytes(kind, layer, c, None)
+            it.run = (lambda it=it: Q.add(it.a, it.case.s_a, it.case.zp_a, it.b, it.case.s_b, it.case.zp_b,
+                                          it.case.s_o, it.case.zp_o, "u8", out=it.out))
+        else:
+            w = torch.from_numpy(c.w).cuda()
+            bias = None if c.bias is None else torch.from_numpy(c.bias).cuda()
+            xdt = "u8" if c.x.dtype == np.uint8 else "i8"
+            if kind == "dense":
+                plan = Q.dense_plan(layer.M, layer.K, xdt, c.s_x, c.zp_x, w, c.s_w, c.zp_w, bias, c.s_y, c.zp_y,
+                                    c.yt, c.act, c.rounding)
+            elif kind == "dw":
+                plan = Q.depthwise_conv2d_plan(c.x.shape, xdt, c.s_x, c.zp_x, w, c.s_w, c.zp_w, bias, c.stride,
+                                               c.pads, 1, c.s_y, c.zp_y, c.yt, c.act, c.rounding)
+            else:
+                plan = Q.conv2d_plan(c.x.shape, xdt, c.s_x, c.zp_x, w, c.s_w, c.zp_w, bias, c.stride, c.pads, 1,
+                                     c.s_y, c.zp_y, c.yt, c.act, c.rounding)
+            it.plan, it.w, it.bias = plan, w, bias
+            it.x = torch.from_numpy(c.x).cuda()
+            it.out = plan.new_output()
+            it.ws = (torch.empty(plan.workspace_size, dtype=torch.uint8, device="cuda")
+                     if plan.workspace_size else None)
+            it.desc = plan.describe()
+            it.macs = _macs(kind, layer, c, plan.out_shape)
+            it.bytes = _bytes(kind, layer, c, plan.out_shape)
+            it.run = (lambda it=it: it.plan.run(it.x, it.out, it.ws))
+        items.append(it)
+        del c
+    return items, batch
+
+
+def kernel_group(it):
+    """Kernel instantiation a layer runs (tile shape and gather width)."""
+    if it.kind == "add":
+        return "add"
+    if it.kind == "dw":
+        return "depthwise"
+    d = dict(kv.split("=") for kv in it.desc.split()[1:] if "=" in kv)
+    return f"conv_mfma tile={d['tile']} gather={d['gather']} split={'1' if d['split'] == '1' else 'k'}"
+
+
+# ------------------------------------------------------------------ timing
+
+def time_steps(items, steps, warmup, use_graph):
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        for it in items:
+            it.run()
+    torch.cuda.synchronize()
+    graph = None
+    if use_graph:
+        try:
+            graph = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(stream)
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(graph, stream=s):
+                    for it in items:
+                        it.run()
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+        except Exception as e:  # capture not possible: time eager launches
+            log(f"graph capture failed ({e}); timing eager launches")
+            graph = None
+            torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            for it in items:
+                it.run()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps, graph is not None
+
+
+def time_launches(items, steps):
+    """Per-launch kernel time: each layer's launch bracketed by events on the
+    stream it runs on (torch's current stream), over `steps` eager steps."""
+    import torch
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in items]
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for s in range(steps):
+        for i, it in enumerate(items):
+            ev[s][i][0].record()
+            it.run()
+            ev[s][i][1].record()
+    torch.cuda.synchronize()
+    per = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # ms
+    return np.median(per, axis=0)
+
+
+# ------------------------------------------------------------------ CPU oracle baseline
+
+def cpu_baseline(workload, target_s=12.0):
+    """The oracle (plain int64 loop nests) on a bounded sample of the same
+    layers: a fixed number of randomly chosen outputs per layer."""
+    from oracle import oracle as O
+    import workloads as W
+
+    layers, _ = _layers(workload)
+    convs = [(k, l, c) for k, l, c in layers if k in ("conv", "dense", "dw")]
+
+    def run(per_layer):
+        macs = 0
+        t0 = time.perf_counter()
+        for i, (kind, layer, c) in enumerate(convs):
+            if kind == "dense":
+                rows = max(1, per_layer // layer.N)
+                xs = c.x[:rows]
+                O.dense_acc(xs, c.zp_x, c.w, c.zp_w, c.bias)
+                macs += rows * layer.N * layer.K
+                continue
+            Ho, Wo = O.conv_out_hw(layer.H, layer.W, layer.R, layer.S, c.stride, c.pads)
+            total = c.x.shape[0] * Ho * Wo * c.K
+            idx = W.sample_indices(total, per_layer, seed=i)
+            acc = O.conv2d_acc_points(c.x, c.zp_x, c.w, idx, c.zp_w, c.bias, c.stride, c.pads, (1, 1),
+                                      c.depthwise)
+            O.requantize_points(acc, idx, c.K, c.s_x, c.s_w, c.s_y, c.zp_y, c.yt, c.act, c.rounding)
+            macs += idx.size * c.J
+        return macs, time.perf_counter() - t0
+
+    m0, t0 = run(64)
+    per = int(64 * max(1.0, target_s / max(t0, 1e-3)))
+    per = min(per, 200000)
+    macs, t = run(per)
+    return {"value": round(2.0 * macs / t / 1e12, 6), "unit": "TOP/s", "cores": O.threads(), "kind": "oracle",
+            "sample": f"{per} randomly chosen outputs of each of the {len(convs)} layers of the same workload "
+                      f"({macs / 1e9:.2f} G MAC in {t:.1f} s, requantize included)"}
+
+
+# ------------------------------------------------------------------ traffic from committed counters
+
+def traffic_for(group):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, if it was taken on the current
+    kernel source (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, "paper_2006_10226_amd", "csrc", "conv_mfma.hip"), "rb").read()
+        if rec.get("source_sha1") != hashlib.sha1(src).hexdigest():
+            return None
+        return rec.get("groups", {}).get(group, {}).get("bytes_per_launch")
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet50_b32")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers-out", default=os.path.join(ROOT, "gpurun_out", "bench_layers.json"))
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    log(f"setting up {args.workload}")
+    items, batch = setup(args.workload)
+    total_macs = sum(it.macs for it in items)
+    total_bytes = sum(it.bytes for it in items)
+    log(f"{len(items)} layers, {total_macs / 1e9:.2f} G MAC per step")
+
+    ms, graphed = time_steps(items, args.steps, args.warmup, not args.no_graph)
+    value = 2.0 * total_macs / (ms * 1e-3) / 1e12
+    log(f"step {ms:.4f} ms -> {value:.1f} TOP/s (graph={graphed})")
+
+    per = time_launches(items, args.steps)
+    groups = {}
+    for it, t in zip(items, per):
+        g = kernel_group(it)
+        d = groups.setdefault(g, {"launches": 0, "ms": 0.0, "macs": 0, "bytes": 0})
+        d["launches"] += 1
+        d["ms"] += float(t)
+        d["macs"] += it.macs
+        d["bytes"] += it.bytes
+    dom = max(groups, key=lambda g: groups[g]["ms"])
+    D = groups[dom]
+    avg_ms = D["ms"] / D["launches"]
+    if D["macs"] > 0:
+        achieved = 2.0 * D["macs"] / D["launches"] / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                "frac": round(achieved / PEAK_INT8_TOPS, 4)}
+    else:
+        achieved = D["bytes"] / D["launches"] / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = traffic_for(dom)
+    roof["kernel"] = dom
+    roof["avg_launch_us"] = round(avg_ms * 1e3, 3)
+    roof["launches_per_step"] = D["launches"]
+
+    layer_rows = []
+    for it, t in zip(items, per):
+        row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3),
+               "gmac": round(it.macs / 1e9, 4), "mbytes": round(it.bytes / 1e6, 3)}
+        if it.macs:
+            row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
+        row["gbs"] = round(it.bytes / (float(t) * 1e-3) / 1e9, 1)
+        layer_rows.append(row)
+    try:
+        os.makedirs(os.path.dirname(args.layers_out), exist_ok=True)
+        with open(args.layers_out, "w") as f:
+            json.dump({"workload": args.workload, "step_ms": ms, "groups": groups, "layers": layer_rows}, f,
+                      indent=1)
+    except OSError:
+        pass
+    for r in layer_rows:
+        log(f"  {r['layer']:<24} {r['us']:9.2f} us  {r.get('tops', 0):8.1f} TOP/s {r['gbs']:8.1f} GB/s  {r['plan']}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(args.workload)
+        log(f"cpu oracle: {cpu}")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic (seeded, architecture shapes only, random weights)",
+        "config": {"workload": args.workload, "batch": batch, "layers": len(items),
+                   "gmac_per_step": round(total_macs / 1e9, 3), "launch": "hipGraph" if graphed else "eager",
+                   "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4)},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -69,8 +69,14 @@ def _load():
     lib.oracle_add.argtypes = [P, i32, f32, i32, P, i32, f32, i32, i64, f32, i32, i32,
                                i64, i64, i32, P]
     lib.oracle_add.restype = ctypes.c_int
+    lib.oracle_threads.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops run on."""
+    return int(_load().oracle_threads())
 
 
 def _ptr(a):

@@ -40,6 +40,7 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <math.h>
+#include <omp.h>
 
 #define ORACLE_U8 0
 #define ORACLE_I8 1
@@ -441,4 +442,16 @@ int oracle_requantize_value(int64_t v, double M, int32_t zp_out, int32_t yt,
                             int64_t lo, int64_t hi, int32_t rounding, int64_t *out)
 {
     return requantize_one(v, M, zp_out, yt, lo, hi, rounding, out);
+}
+
+/* Number of OpenMP threads the oracle's parallel loops use. */
+int oracle_threads(void)
+{
+    int n = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        n = omp_get_num_threads();
+    }
+    return n;
 }

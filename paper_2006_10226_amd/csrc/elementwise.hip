@@ -1,0 +1,318 @@
+// Bandwidth-bound kernels: depthwise conv2d (VALU), standalone requantize
+// and qnn.add.
+//
+// Depthwise (channel multiplier 1) uses the subtract-first form of the
+// quantized conv (Sec. III-B, the alternative lowering): each tap
+// contributes (x - zp_x) * (w - zp_w[c]) in int32, padded taps contribute
+// nothing.  With 9 products per output this is far from any MFMA shape and
+// is bound by HBM traffic, so it runs on the vector ALUs.
+//
+// Requantize is Eq. (5) with the fixed-point multiplier of Sec. III-B; add
+// requantizes each operand to the output scale and sums them.
+#include "qnn_internal.h"
+
+namespace qnn {
+
+__device__ __forceinline__ long long rms(int v, int mult, int shift, int rounding)
+{
+    long long p = (long long)v * (long long)mult;
+    long long half = 1LL << (shift - 1);
+    if (rounding == 0)
+        return (p + half) >> shift;
+    long long a = p < 0 ? -p : p;
+    long long t = (a + half) >> shift;
+    return p < 0 ? -t : t;
+}
+
+__device__ __forceinline__ int clampll(long long v, int lo, int hi)
+{
+    return (int)(v < lo ? lo : (v > hi ? hi : v));
+}
+
+// ------------------------------------------------------------- depthwise
+
+template <bool VEC4, bool OUT_I32>
+__global__ void __launch_bounds__(256) depthwise_kernel(DwArgs a)
+{
+    const int CV = VEC4 ? 4 : 1;
+    const int groups = a.C / CV;
+    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long long total = (long long)a.N * a.Ho * a.Wo * groups;
+    if (gid >= total)
+        return;
+    const int g = (int)(gid % groups);
+    const int m = (int)(gid / groups);
+    const int ow = m % a.Wo, t = m / a.Wo, oh = t % a.Ho, n = t / a.Ho;
+    const int c = g * CV;
+    int acc[CV];
+#pragma unroll
+    for (int e = 0; e < CV; ++e)
+        acc[e] = 0;
+    for (int r = 0; r < a.R; ++r) {
+        const int ih = oh * a.sh - a.pt + r * a.dh;
+        if ((unsigned)ih >= (unsigned)a.H)
+            continue;
+        for (int s = 0; s < a.S; ++s) {
+            const int iw = ow * a.sw - a.pl + s * a.dw;
+            if ((unsigned)iw >= (unsigned)a.W)
+                continue;
+            const uint8_t *src = a.x + ((size_t)(n * a.H + ih) * a.W + iw) * a.C + c;
+            const int32_t *wt = a.wq + (r * a.S + s) * a.C + c;
+            if constexpr (VEC4) {
+                const uint32_t xv = *(const uint32_t *)src;
+                const int4 wv = *(const int4 *)wt;
+                const int wk[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t b = (xv >> (8 * e)) & 0xffu;
+                    const int xi = a.x_signed ? (int)(int8_t)b : (int)b;
+                    acc[e] += (xi - a.zp_x) * wk[e];
+                }
+            } else {
+                const int xi = a.x_signed ? (int)(int8_t)src[0] : (int)src[0];
+                acc[0] += (xi - a.zp_x) * wt[0];
+            }
+        }
+    }
+    const size_t off = (size_t)m * a.y_ldc + a.y_coff + c;
+    if constexpr (OUT_I32) {
+        int32_t *yp = (int32_t *)a.y + off;
+#pragma unroll
+        for (int e = 0; e < CV; ++e)
+            yp[e] = (int)((uint32_t)acc[e] + (uint32_t)a.chan[c + e].bconst);
+    } else {
+        uint8_t *yp = (uint8_t *)a.y + off;
+#pragma unroll
+        for (int e = 0; e < CV; ++e) {
+            const ChanRec cr = a.chan[c + e];
+            const int v = (int)((uint32_t)acc[e] + (uint32_t)cr.bconst);
+            yp[e] = (uint8_t)clampll(rms(v, cr.mult, cr.shift, a.rounding) + a.zp_y, a.lo, a.hi);
+        }
+    }
+}
+
+// wq[t][c] = w[t][c] - zp_w[c]; chan[c].bconst = bias[c].
+__global__ void __launch_bounds__(256) prep_dw_kernel(const int8_t *w, const int32_t *bias, int RS, int C,
+                                                      int32_t *wq, ChanRec *chan)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= RS * C)
+        return;
+    const int c = i % C;
+    wq[i] = (int)w[i] - chan[c].zpw;
+    if (i < C)
+        chan[c].bconst = bias ? bias[c] : 0;
+}
+
+hipError_t launch_prep_dw(const int8_t *w, const int32_t *bias, int RS, int C, int32_t *wq, ChanRec *chan,
+                          hipStream_t st)
+{
+    const int n = RS * C;
+    hipLaunchKernelGGL(prep_dw_kernel, dim3((n + 255) / 256), dim3(256), 0, st, w, bias, RS, C, wq, chan);
+    return hipGetLastError();
+}
+
+hipError_t launch_depthwise(const DwArgs &a, hipStream_t st)
+{
+    const bool vec = (a.C % 4 == 0) && (a.y_ldc % 4 == 0) && (a.y_coff % 4 == 0) &&
+                     (((uintptr_t)a.x & 3) == 0);
+    const long long total = (long long)a.N * a.Ho * a.Wo * (vec ? a.C / 4 : a.C);
+    dim3 grid((unsigned)((total + 255) / 256)), block(256);
+    if (vec) {
+        if (a.out_i32) hipLaunchKernelGGL((depthwise_kernel<true, true>), grid, block, 0, st, a);
+        else hipLaunchKernelGGL((depthwise_kernel<true, false>), grid, block, 0, st, a);
+    } else {
+        if (a.out_i32) hipLaunchKernelGGL((depthwise_kernel<false, true>), grid, block, 0, st, a);
+        else hipLaunchKernelGGL((depthwise_kernel<false, false>), grid, block, 0, st, a);
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------- elementwise
+
+// dtype codes: 0 uint8, 1 int8, 2 int32
+template <int DT>
+__device__ __forceinline__ int ld(const void *p, long long i)
+{
+    if constexpr (DT == 0) return ((const uint8_t *)p)[i];
+    else if constexpr (DT == 1) return ((const int8_t *)p)[i];
+    else return ((const int32_t *)p)[i];
+}
+
+template <int DT>
+__device__ __forceinline__ void st(void *p, long long i, int v)
+{
+    if constexpr (DT == 0) ((uint8_t *)p)[i] = (uint8_t)v;
+    else if constexpr (DT == 1) ((int8_t *)p)[i] = (int8_t)v;
+    else ((int32_t *)p)[i] = v;
+}
+
+// Load 16 consecutive elements starting at a 16-element aligned index.
+template <int DT>
+__device__ __forceinline__ void ld16(const void *p, long long i0, int v[16])
+{
+    if constexpr (DT == 2) {
+        const int4 *q = (const int4 *)((const int32_t *)p + i0);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int4 u = q[k];
+            v[4 * k] = u.x; v[4 * k + 1] = u.y; v[4 * k + 2] = u.z; v[4 * k + 3] = u.w;
+        }
+    } else {
+        const int4 u = *(const int4 *)((const uint8_t *)p + i0);
+        const uint32_t w[4] = {(uint32_t)u.x, (uint32_t)u.y, (uint32_t)u.z, (uint32_t)u.w};
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const uint32_t b = (w[k >> 2] >> (8 * (k & 3))) & 0xffu;
+            v[k] = DT == 1 ? (int)(int8_t)b : (int)b;
+        }
+    }
+}
+
+template <int DT>
+__device__ __forceinline__ void st16(void *p, long long i0, const int v[16])
+{
+    if constexpr (DT == 2) {
+        int4 *q = (int4 *)((int32_t *)p + i0);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            q[k] = make_int4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
+    } else {
+        uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+            w[k >> 2] |= ((uint32_t)v[k] & 0xffu) << (8 * (k & 3));
+        *(int4 *)((uint8_t *)p + i0) = make_int4(w[0], w[1], w[2], w[3]);
+    }
+}
+
+__device__ __forceinline__ int req_one(const ReqArgs &a, int q, int c)
+{
+    int mult = a.mult, shift = a.shift, zi = a.zp_in, zo = a.zp_out;
+    if (a.tab) {
+        const int4 t = *(const int4 *)(a.tab + 4 * c);
+        mult = t.x; shift = t.y; zi = t.z; zo = t.w;
+    }
+    return clampll(rms(q - zi, mult, shift, a.rounding) + zo, a.lo, a.hi);
+}
+
+// Each thread handles groups of 16 elements (vector loads/stores when the
+// buffers allow it), grid-stride.
+template <int XDT, int YDT, bool VEC>
+__global__ void __launch_bounds__(256) requantize_kernel(ReqArgs a)
+{
+    const long long ngroups = (a.count + 15) / 16;
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    for (long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x; g < ngroups; g += stride) {
+        const long long i0 = g * 16;
+        int c = a.tab ? (int)(i0 % a.channels) : 0;
+        if (VEC && i0 + 16 <= a.count) {
+            int v[16];
+            ld16<XDT>(a.x, i0, v);
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                v[k] = req_one(a, v[k], c);
+                if (a.tab && ++c == a.channels)
+                    c = 0;
+            }
+            st16<YDT>(a.y, i0, v);
+        } else {
+            for (long long i = i0; i < i0 + 16 && i < a.count; ++i) {
+                st<YDT>(a.y, i, req_one(a, ld<XDT>(a.x, i), c));
+                if (a.tab && ++c == a.channels)
+                    c = 0;
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ int add_one(const AddArgs &a, int x, int y)
+{
+    const long long t = rms(x - a.zpa, a.ma, a.na, a.rounding) + rms(y - a.zpb, a.mb, a.nb, a.rounding);
+    return clampll(t + a.zp_y, a.lo, a.hi);
+}
+
+template <int ADT, int BDT, int YDT, bool VEC>
+__global__ void __launch_bounds__(256) add_kernel(AddArgs a)
+{
+    const long long ngroups = (a.count + 15) / 16;
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    for (long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x; g < ngroups; g += stride) {
+        const long long i0 = g * 16;
+        if (VEC && i0 + 16 <= a.count) {
+            int u[16], v[16];
+            ld16<ADT>(a.a, i0, u);
+            ld16<BDT>(a.b, i0, v);
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                u[k] = add_one(a, u[k], v[k]);
+            st16<YDT>(a.y, i0, u);
+        } else {
+            for (long long i = i0; i < i0 + 16 && i < a.count; ++i)
+                st<YDT>(a.y, i, add_one(a, ld<ADT>(a.a, i), ld<BDT>(a.b, i)));
+        }
+    }
+}
+
+static dim3 ew_grid(long long count)
+{
+    const long long groups = (count + 15) / 16;
+    long long blocks = (groups + 255) / 256;
+    const long long cap = 256LL * 32;  // enough resident waves to saturate HBM
+    if (blocks > cap) blocks = cap;
+    if (blocks < 1) blocks = 1;
+    return dim3((unsigned)blocks);
+}
+
+template <int XDT, int YDT>
+static void req_launch(const ReqArgs &a, bool vec, hipStream_t s)
+{
+    if (vec) hipLaunchKernelGGL((requantize_kernel<XDT, YDT, true>), ew_grid(a.count), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((requantize_kernel<XDT, YDT, false>), ew_grid(a.count), dim3(256), 0, s, a);
+}
+
+template <int XDT>
+static void req_launch_y(const ReqArgs &a, int ydt, bool vec, hipStream_t s)
+{
+    if (ydt == 0) req_launch<XDT, 0>(a, vec, s);
+    else if (ydt == 1) req_launch<XDT, 1>(a, vec, s);
+    else req_launch<XDT, 2>(a, vec, s);
+}
+
+hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, hipStream_t s)
+{
+    if (xdt == 0) req_launch_y<0>(a, ydt, aligned, s);
+    else if (xdt == 1) req_launch_y<1>(a, ydt, aligned, s);
+    else req_launch_y<2>(a, ydt, aligned, s);
+    return hipGetLastError();
+}
+
+template <int ADT, int BDT, int YDT>
+static void add_launch(const AddArgs &a, bool vec, hipStream_t s)
+{
+    if (vec) hipLaunchKernelGGL((add_kernel<ADT, BDT, YDT, true>), ew_grid(a.count), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((add_kernel<ADT, BDT, YDT, false>), ew_grid(a.count), dim3(256), 0, s, a);
+}
+
+template <int ADT, int BDT>
+static void add_launch_y(const AddArgs &a, int ydt, bool vec, hipStream_t s)
+{
+    if (ydt == 0) add_launch<ADT, BDT, 0>(a, vec, s);
+    else add_launch<ADT, BDT, 1>(a, vec, s);
+}
+
+template <int ADT>
+static void add_launch_b(const AddArgs &a, int bdt, int ydt, bool vec, hipStream_t s)
+{
+    if (bdt == 0) add_launch_y<ADT, 0>(a, ydt, vec, s);
+    else add_launch_y<ADT, 1>(a, ydt, vec, s);
+}
+
+hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned, hipStream_t s)
+{
+    if (adt == 0) add_launch_b<0>(a, bdt, ydt, aligned, s);
+    else add_launch_b<1>(a, bdt, ydt, aligned, s);
+    return hipGetLastError();
+}
+
+}  // namespace qnn

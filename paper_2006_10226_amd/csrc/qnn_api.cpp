@@ -1,0 +1,858 @@
+// C ABI of libqnn: argument validation, plan creation (per-channel
+// fixed-point multipliers, folded constants, packed weights), kernel choice
+// and launches.  See include/qnn.h for the contract of every entry point.
+#include "qnn.h"
+#include "qnn_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace qnn;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+qnn_status fail(qnn_status s, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+qnn_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(QNN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr)                                 \
+    do {                                              \
+        hipError_t e_ = (expr);                       \
+        if (e_ != hipSuccess)                         \
+            return hip_fail(e_, #expr);               \
+    } while (0)
+
+struct Range {
+    int64_t lo, hi;
+};
+
+bool dtype_range(qnn_dtype t, Range *r)
+{
+    switch (t) {
+    case QNN_UINT8: *r = {0, 255}; return true;
+    case QNN_INT8: *r = {-128, 127}; return true;
+    case QNN_INT32: *r = {INT32_MIN, INT32_MAX}; return true;
+    default: return false;
+    }
+}
+
+const char *dtype_name(qnn_dtype t)
+{
+    switch (t) {
+    case QNN_UINT8: return "uint8";
+    case QNN_INT8: return "int8";
+    case QNN_INT32: return "int32";
+    default: return "?";
+    }
+}
+
+// Fixed-point multiplier of Sec. III-B (the library's own derivation; see
+// qnn_quantize_multiplier in qnn.h for the rule).
+bool derive_multiplier(double M, int32_t *mult, int32_t *shift)
+{
+    if (!(M >= 0.0) || !std::isfinite(M))
+        return false;
+    if (M == 0.0) {
+        *mult = 0;
+        *shift = 1;
+        return true;
+    }
+    int e;
+    const double f = std::frexp(M, &e);
+    int64_t q = (int64_t)std::floor(std::ldexp(f, 31) + 0.5);
+    if (q == (int64_t(1) << 31)) {
+        q >>= 1;
+        ++e;
+    }
+    const int n = 31 - e;
+    if (n < 1)
+        return false;
+    *mult = (int32_t)q;
+    *shift = n;
+    return true;
+}
+
+qnn_status check_qparams(const qnn_qparams &q, const char *what, int32_t n_allowed, qnn_dtype zp_dtype,
+                         bool allow_zero_scale)
+{
+    if (!q.scale || !q.zero_point)
+        return fail(QNN_ERR_NULL, "%s: scale / zero_point array is NULL", what);
+    if (q.n != 1 && q.n != n_allowed)
+        return fail(QNN_ERR_QPARAM, "%s: qparams length %d, expected 1 or %d", what, q.n, n_allowed);
+    Range r;
+    dtype_range(zp_dtype, &r);
+    for (int i = 0; i < q.n; ++i) {
+        const float s = q.scale[i];
+        if (!std::isfinite(s) || s < 0.0f || (s == 0.0f && !allow_zero_scale))
+            return fail(QNN_ERR_QPARAM, "%s: scale[%d] = %g is not a finite positive value", what, i, (double)s);
+        if (q.zero_point[i] < r.lo || q.zero_point[i] > r.hi)
+            return fail(QNN_ERR_QPARAM, "%s: zero_point[%d] = %d outside the %s range", what, i, q.zero_point[i],
+                        dtype_name(zp_dtype));
+    }
+    return QNN_OK;
+}
+
+// Output clamp intersected with the output dtype range.
+qnn_status out_bounds(qnn_dtype yt, qnn_clamp act, int32_t *lo, int32_t *hi)
+{
+    Range r;
+    if (!dtype_range(yt, &r))
+        return fail(QNN_ERR_DTYPE, "unknown output dtype %d", (int)yt);
+    const int64_t l = std::max<int64_t>(r.lo, act.lo), h = std::min<int64_t>(r.hi, act.hi);
+    if (l > h)
+        return fail(QNN_ERR_QPARAM, "empty output clamp [%d, %d] for %s", act.lo, act.hi, dtype_name(yt));
+    *lo = (int32_t)l;
+    *hi = (int32_t)h;
+    return QNN_OK;
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *v = std::getenv(name);
+    return v && *v ? std::atoi(v) : dflt;
+}
+
+enum PlanKind { PLAN_CONV = 0, PLAN_DW = 1, PLAN_REQ = 2 };
+
+}  // namespace
+
+struct qnn_plan {
+    PlanKind kind;
+    // conv / dense
+    ConvArgs conv{};
+    int tile = 0, avec = 16, mode = OUT_REQUANT;
+    bool term3 = false;
+    size_t ws_partial_bytes = 0, ws_asum_bytes = 0;
+    // depthwise
+    DwArgs dw{};
+    // requantize
+    ReqArgs req{};
+    int xdt = 0, ydt = 0;
+    // memory
+    void *dev = nullptr;      // packed weights + tables
+    void *ws_own = nullptr;   // plan-owned workspace
+    size_t ws_bytes = 0;
+    std::string desc;
+};
+
+namespace {
+
+void free_plan(qnn_plan *p)
+{
+    if (!p)
+        return;
+    if (p->dev)
+        (void)hipFree(p->dev);
+    if (p->ws_own)
+        (void)hipFree(p->ws_own);
+    delete p;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct ConvDesc {
+    qnn_dtype xt;
+    int32_t N, H, W, C;
+    qnn_qparams xq;
+    const int8_t *w;
+    int32_t K, R, S;
+    qnn_qparams wq;
+    const int32_t *bias;
+    qnn_conv_params cp;
+    qnn_dtype yt;
+    qnn_qparams yq;
+    qnn_clamp act;
+    qnn_rounding rnd;
+    int32_t y_ldc, y_coff;
+    bool depthwise;
+};
+
+// Shared validation of conv / depthwise / dense descriptors.  Fills the
+// output size, output clamp and per-channel multipliers.
+qnn_status validate_conv(const ConvDesc &d, int32_t *Ho, int32_t *Wo, int32_t *lo, int32_t *hi,
+                         std::vector<int32_t> *mult, std::vector<int32_t> *shift)
+{
+    const char *op = d.depthwise ? "depthwise_conv2d" : "conv2d";
+    if (d.xt != QNN_UINT8 && d.xt != QNN_INT8)
+        return fail(QNN_ERR_DTYPE, "%s: input dtype must be uint8 or int8", op);
+    if (d.yt != QNN_UINT8 && d.yt != QNN_INT8 && d.yt != QNN_INT32)
+        return fail(QNN_ERR_DTYPE, "%s: output dtype must be uint8, int8 or int32", op);
+    if (d.rnd != QNN_ROUND_HALF_UP && d.rnd != QNN_ROUND_HALF_AWAY)
+        return fail(QNN_ERR_QPARAM, "%s: unknown rounding %d", op, (int)d.rnd);
+    if (d.N < 0 || d.H < 1 || d.W < 1 || d.C < 1 || d.K < 1 || d.R < 1 || d.S < 1)
+        return fail(QNN_ERR_SHAPE, "%s: sizes must be positive (N >= 0)", op);
+    const qnn_conv_params &c = d.cp;
+    if (c.stride_h < 1 || c.stride_w < 1 || c.dil_h < 1 || c.dil_w < 1 || c.pad_top < 0 || c.pad_left < 0 ||
+        c.pad_bottom < 0 || c.pad_right < 0)
+        return fail(QNN_ERR_SHAPE, "%s: strides/dilations must be >= 1 and pads >= 0", op);
+    const int64_t hn = (int64_t)d.H + c.pad_top + c.pad_bottom - (int64_t)c.dil_h * (d.R - 1) - 1;
+    const int64_t wn = (int64_t)d.W + c.pad_left + c.pad_right - (int64_t)c.dil_w * (d.S - 1) - 1;
+    if (hn < 0 || wn < 0)
+        return fail(QNN_ERR_SHAPE, "%s: filter larger than the padded input", op);
+    *Ho = (int32_t)(hn / c.stride_h + 1);
+    *Wo = (int32_t)(wn / c.stride_w + 1);
+    if (d.y_coff < 0 || (int64_t)d.y_ldc < (int64_t)d.y_coff + d.K)
+        return fail(QNN_ERR_SHAPE, "%s: need y_coff >= 0 and y_ldc >= y_coff + %d (got %d, %d)", op, d.K,
+                    d.y_ldc, d.y_coff);
+    const int64_t xelems = (int64_t)d.N * d.H * d.W * d.C;
+    const int64_t M = (int64_t)d.N * *Ho * *Wo;
+    if (xelems >= (int64_t(1) << 31) || M * d.y_ldc >= (int64_t(1) << 31) ||
+        (int64_t)d.R * d.S * d.C >= (int64_t(1) << 24))
+        return fail(QNN_ERR_UNSUPPORTED, "%s: tensors of 2^31 or more elements are not supported", op);
+    if (!d.w)
+        return fail(QNN_ERR_NULL, "%s: weight pointer is NULL", op);
+
+    qnn_status s;
+    if ((s = check_qparams(d.xq, "x qparams", 1, d.xt, false)) != QNN_OK)
+        return s;
+    if ((s = check_qparams(d.wq, "w qparams", d.K, QNN_INT8, true)) != QNN_OK)
+        return s;
+    *lo = INT32_MIN;
+    *hi = INT32_MAX;
+    mult->assign(d.K, 0);
+    shift->assign(d.K, 1);
+    if (d.yt != QNN_INT32) {
+        if ((s = check_qparams(d.yq, "y qparams", 1, d.yt, false)) != QNN_OK)
+            return s;
+        if ((s = out_bounds(d.yt, d.act, lo, hi)) != QNN_OK)
+            return s;
+        for (int k = 0; k < d.K; ++k) {
+            const double sw = (double)d.wq.scale[d.wq.n == 1 ? 0 : k];
+            const double Mk = ((double)d.xq.scale[0] * sw) / (double)d.yq.scale[0];
+            int32_t m, n;
+            if (!derive_multiplier(Mk, &m, &n))
+                return fail(QNN_ERR_QPARAM, "%s: requantize multiplier %g of channel %d is out of range", op, Mk, k);
+            (*mult)[k] = m;
+            (*shift)[k] = n > 63 ? 63 : n;
+        }
+    }
+    return QNN_OK;
+}
+
+// Accumulator bound (host copy of the bias): J * max|x - zp_x| * max|w - zp_w| + |bias| < 2^31.
+qnn_status check_overflow(const ConvDesc &d, int64_t J, const std::vector<int32_t> &bias_h)
+{
+    Range xr;
+    dtype_range(d.xt, &xr);
+    const int64_t zx = d.xq.zero_point[0];
+    const int64_t ax = std::max(zx - xr.lo, xr.hi - zx);
+    for (int k = 0; k < d.K; ++k) {
+        const int64_t zw = d.wq.zero_point[d.wq.n == 1 ? 0 : k];
+        const int64_t aw = std::max(zw + 128, 127 - zw);
+        const int64_t b = bias_h.empty() ? 0 : std::llabs((long long)bias_h[k]);
+        if (J * ax * aw + b >= (int64_t(1) << 31))
+            return fail(QNN_ERR_OVERFLOW,
+                        "accumulator bound J*|x-zp|*|w-zp|+|bias| = %lld for channel %d does not fit int32",
+                        (long long)(J * ax * aw + b), k);
+    }
+    return QNN_OK;
+}
+
+qnn_status read_bias(const int32_t *bias, int n, hipStream_t st, std::vector<int32_t> *out)
+{
+    out->clear();
+    if (!bias)
+        return QNN_OK;
+    out->resize(n);
+    HIP_TRY(hipMemcpyAsync(out->data(), bias, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    return QNN_OK;
+}
+
+// Tile and split-K choice for an implicit-GEMM problem of M pixels x K
+// channels x J reduction.
+void choose_tiling(int64_t M, int K, int J, int *tile, int *nsplit, int *ksteps, int *tiles_c, int *nblocks,
+                   int *Kpad, int *Jpad)
+{
+    int t = env_int("QNN_TILE", -1);
+    if (t < 0 || t >= TILE_COUNT) {
+        const int64_t big = (M + 127) / 128 * ((K + 127) / 128);
+        if (big < 160)
+            t = TILE_64x64;
+        else if (K <= 64)
+            t = TILE_64x256;
+        else
+            t = TILE_128x128;
+    }
+    const TileShape ts = tile_shape(t);
+    *tile = t;
+    *Kpad = (int)align_up(K, ts.tc);
+    *Jpad = (int)align_up(J, ts.bk);
+    *tiles_c = *Kpad / ts.tc;
+    const int64_t tiles_p = (M + ts.tp - 1) / ts.tp;
+    *nblocks = (int)(*tiles_c * tiles_p);
+    const int nk = *Jpad / ts.bk;
+    int ns = env_int("QNN_SPLIT", 0);
+    if (ns <= 0) {
+        ns = 1;
+        if (*nblocks > 0 && *nblocks < 256 && nk >= 4) {
+            ns = (int)((512 + *nblocks - 1) / *nblocks);
+            ns = std::min(ns, nk / 2);
+            ns = std::min(ns, 16);
+            ns = std::max(ns, 1);
+        }
+    }
+    ns = std::min(ns, nk);
+    *ksteps = (nk + ns - 1) / ns;
+    *nsplit = (nk + *ksteps - 1) / *ksteps;
+}
+
+qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
+{
+    int32_t Ho, Wo, lo, hi;
+    std::vector<int32_t> mult, shift;
+    qnn_status s = validate_conv(d, &Ho, &Wo, &lo, &hi, &mult, &shift);
+    if (s != QNN_OK)
+        return s;
+    std::vector<int32_t> bias_h;
+    if ((s = read_bias(d.bias, d.K, st, &bias_h)) != QNN_OK)
+        return s;
+    const int64_t J = d.depthwise ? (int64_t)d.R * d.S : (int64_t)d.R * d.S * d.C;
+    if ((s = check_overflow(d, J, bias_h)) != QNN_OK)
+        return s;
+
+    qnn_plan *p = new (std::nothrow) qnn_plan();
+    if (!p)
+        return fail(QNN_ERR_ALLOC, "out of host memory");
+    const int32_t zpx = d.xq.zero_point[0];
+    const int64_t M = (int64_t)d.N * Ho * Wo;
+
+    if (d.depthwise) {
+        p->kind = PLAN_DW;
+        const int C = d.C, RS = d.R * d.S;
+        const size_t wq_bytes = align_up(sizeof(int32_t) * RS * C, 256);
+        const size_t ch_bytes = sizeof(ChanRec) * C;
+        hipError_t e = hipMalloc(&p->dev, wq_bytes + ch_bytes);
+        if (e != hipSuccess) {
+            free_plan(p);
+            return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", wq_bytes + ch_bytes);
+        }
+        int32_t *wq = (int32_t *)p->dev;
+        ChanRec *chan = (ChanRec *)((char *)p->dev + wq_bytes);
+        std::vector<ChanRec> ch(C);
+        for (int c = 0; c < C; ++c)
+            ch[c] = ChanRec{mult[c], shift[c], 0, d.wq.zero_point[d.wq.n == 1 ? 0 : c]};
+        if ((e = hipMemcpyAsync(chan, ch.data(), ch_bytes, hipMemcpyHostToDevice, st)) != hipSuccess ||
+            (e = launch_prep_dw(d.w, d.bias, RS, C, wq, chan, st)) != hipSuccess ||
+            (e = hipStreamSynchronize(st)) != hipSuccess) {
+            free_plan(p);
+            return hip_fail(e, "depthwise plan preparation");
+        }
+        DwArgs &a = p->dw;
+        a.wq = wq;
+        a.chan = chan;
+        a.N = d.N; a.H = d.H; a.W = d.W; a.C = d.C; a.Ho = Ho; a.Wo = Wo; a.R = d.R; a.S = d.S;
+        a.sh = d.cp.stride_h; a.sw = d.cp.stride_w; a.pt = d.cp.pad_top; a.pl = d.cp.pad_left;
+        a.dh = d.cp.dil_h; a.dw = d.cp.dil_w;
+        a.zp_x = zpx;
+        a.x_signed = d.xt == QNN_INT8;
+        a.ydt = d.yt; a.lo = lo; a.hi = hi;
+        a.zp_y = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
+        a.rounding = d.rnd;
+        a.y_ldc = d.y_ldc; a.y_coff = d.y_coff;
+        a.out_i32 = d.yt == QNN_INT32;
+        char buf[128];
+        snprintf(buf, sizeof buf, "depthwise %dx%d stride %dx%d M=%lld C=%d", d.R, d.S, a.sh, a.sw, (long long)M, C);
+        p->desc = buf;
+        *out = p;
+        return QNN_OK;
+    }
+
+    p->kind = PLAN_CONV;
+    int tile, nsplit, ksteps, tiles_c, nblocks, Kpad, Jpad;
+    choose_tiling(M, d.K, (int)J, &tile, &nsplit, &ksteps, &tiles_c, &nblocks, &Kpad, &Jpad);
+    const bool term3 = [&] {
+        for (int i = 0; i < d.wq.n; ++i)
+            if (d.wq.zero_point[i] != 0)
+                return true;
+        return false;
+    }();
+    // legalisation (Sec. III-C): uint8 activations become int8 by x - 128
+    const int32_t zpx_l = d.xt == QNN_UINT8 ? zpx - 128 : zpx;
+    const size_t wp_bytes = align_up((size_t)Kpad * Jpad, 256);
+    const size_t ch_bytes = sizeof(ChanRec) * Kpad;
+    hipError_t e = hipMalloc(&p->dev, wp_bytes + ch_bytes);
+    if (e != hipSuccess) {
+        free_plan(p);
+        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", wp_bytes + ch_bytes);
+    }
+    int8_t *wp = (int8_t *)p->dev;
+    ChanRec *chan = (ChanRec *)((char *)p->dev + wp_bytes);
+    std::vector<ChanRec> ch(Kpad, ChanRec{0, 1, 0, 0});
+    for (int k = 0; k < d.K; ++k)
+        ch[k] = ChanRec{mult[k], shift[k], 0, d.wq.zero_point[d.wq.n == 1 ? 0 : k]};
+    if ((e = hipMemcpyAsync(chan, ch.data(), ch_bytes, hipMemcpyHostToDevice, st)) != hipSuccess ||
+        (e = launch_prep_conv(d.w, d.bias, d.K, (int)J, Jpad, Kpad, zpx_l, wp, chan, st)) != hipSuccess ||
+        (e = hipStreamSynchronize(st)) != hipSuccess) {
+        free_plan(p);
+        return hip_fail(e, "conv plan preparation");
+    }
+
+    ConvArgs &a = p->conv;
+    a.wp = wp;
+    a.chan = chan;
+    a.N = d.N; a.H = d.H; a.W = d.W; a.C = d.C; a.Ho = Ho; a.Wo = Wo; a.R = d.R; a.S = d.S;
+    a.sh = d.cp.stride_h; a.sw = d.cp.stride_w; a.pt = d.cp.pad_top; a.pl = d.cp.pad_left;
+    a.dh = d.cp.dil_h; a.dw = d.cp.dil_w;
+    a.K = d.K; a.Kpad = Kpad; a.J = (int)J; a.Jpad = Jpad; a.M = (int)M;
+    a.flip4 = d.xt == QNN_UINT8 ? 0x80808080u : 0u;
+    const uint32_t pb = (uint32_t)(uint8_t)(int8_t)zpx_l;
+    a.pad4 = pb | (pb << 8) | (pb << 16) | (pb << 24);
+    a.ydt = d.yt;
+    a.lo = lo; a.hi = hi;
+    a.zp_y = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
+    a.rounding = d.rnd;
+    a.y_ldc = d.y_ldc; a.y_coff = d.y_coff;
+    a.vec_store = (d.y_ldc % 4 == 0) && (d.y_coff % 4 == 0);
+    a.ksteps = ksteps;
+    a.nsplit = nsplit;
+    a.tiles_c = tiles_c;
+    a.nblocks = nblocks;
+    p->tile = tile;
+    p->avec = gather_width(d.C);
+    p->mode = d.yt == QNN_INT32 ? OUT_INT32 : OUT_REQUANT;
+    p->term3 = term3;
+    p->ws_partial_bytes = nsplit > 1 ? align_up((size_t)nsplit * M * Kpad * sizeof(int32_t), 256) : 0;
+    p->ws_asum_bytes = term3 ? align_up((size_t)M * sizeof(int32_t), 256) : 0;
+    p->ws_bytes = p->ws_partial_bytes + p->ws_asum_bytes;
+    const TileShape ts = tile_shape(tile);
+    char buf[160];
+    snprintf(buf, sizeof buf, "conv_mfma tile=%dx%dx%d gather=%d split=%d blocks=%d term3=%d M=%lld K=%d J=%lld",
+             ts.tc, ts.tp, ts.bk, p->avec, nsplit, nblocks, (int)term3, (long long)M, d.K, (long long)J);
+    p->desc = buf;
+    *out = p;
+    return QNN_OK;
+}
+
+qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *ws)
+{
+    switch (p->kind) {
+    case PLAN_CONV: {
+        ConvArgs a = p->conv;
+        if (a.M == 0)
+            return QNN_OK;
+        if (!x || !y)
+            return fail(QNN_ERR_NULL, "plan_run: x or y is NULL");
+        a.x = (const uint8_t *)x;
+        a.y = y;
+        if (p->ws_bytes) {
+            if (!ws)
+                ws = p->ws_own;
+            if (!ws)
+                return fail(QNN_ERR_NULL, "plan_run: the plan needs a workspace");
+            a.ws = p->ws_partial_bytes ? (int32_t *)ws : nullptr;
+            a.asum = p->term3 ? (const int32_t *)((char *)ws + p->ws_partial_bytes) : nullptr;
+        }
+        if (((uintptr_t)x & 15) != 0 && p->avec == 16)
+            return fail(QNN_ERR_UNSUPPORTED, "plan_run: x must be 16-byte aligned for C %% 16 == 0");
+        if (((uintptr_t)x & 3) != 0 && p->avec == 4)
+            return fail(QNN_ERR_UNSUPPORTED, "plan_run: x must be 4-byte aligned for C %% 4 == 0");
+        if (a.vec_store && ((uintptr_t)y & (p->mode == OUT_INT32 ? 15 : 3)) != 0)
+            a.vec_store = 0;
+        hipError_t e;
+        if (p->term3 && (e = launch_window_sums(a, (int32_t *)a.asum, st)) != hipSuccess)
+            return hip_fail(e, "window-sum launch");
+        if (a.nsplit > 1) {
+            if ((e = launch_conv(a, p->tile, p->avec, OUT_PARTIAL, st)) != hipSuccess)
+                return hip_fail(e, "conv launch");
+            if ((e = launch_splitk_reduce(a, p->mode, st)) != hipSuccess)
+                return hip_fail(e, "split-K reduce launch");
+        } else if ((e = launch_conv(a, p->tile, p->avec, p->mode, st)) != hipSuccess) {
+            return hip_fail(e, "conv launch");
+        }
+        return QNN_OK;
+    }
+    case PLAN_DW: {
+        DwArgs a = p->dw;
+        if ((int64_t)a.N * a.Ho * a.Wo == 0)
+            return QNN_OK;
+        if (!x || !y)
+            return fail(QNN_ERR_NULL, "plan_run: x or y is NULL");
+        a.x = (const uint8_t *)x;
+        a.y = y;
+        hipError_t e = launch_depthwise(a, st);
+        return e == hipSuccess ? QNN_OK : hip_fail(e, "depthwise launch");
+    }
+    case PLAN_REQ: {
+        ReqArgs a = p->req;
+        if (a.count == 0)
+            return QNN_OK;
+        if (!x || !y)
+            return fail(QNN_ERR_NULL, "plan_run: x or y is NULL");
+        a.x = x;
+        a.y = y;
+        const bool aligned = ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 15) == 0;
+        hipError_t e = launch_requantize(a, p->xdt, p->ydt, aligned, st);
+        return e == hipSuccess ? QNN_OK : hip_fail(e, "requantize launch");
+    }
+    }
+    return fail(QNN_ERR_UNSUPPORTED, "unknown plan kind");
+}
+
+qnn_status alloc_ws(qnn_plan *p)
+{
+    if (!p->ws_bytes)
+        return QNN_OK;
+    if (hipMalloc(&p->ws_own, p->ws_bytes) != hipSuccess)
+        return fail(QNN_ERR_ALLOC, "hipMalloc of a %zu-byte workspace failed", p->ws_bytes);
+    return QNN_OK;
+}
+
+qnn_status one_shot(const ConvDesc &d, hipStream_t st, const void *x, void *y)
+{
+    {
+        // empty input: validate the arguments, then nothing to do
+        int32_t Ho, Wo, lo, hi;
+        std::vector<int32_t> mult, shift;
+        qnn_status s = validate_conv(d, &Ho, &Wo, &lo, &hi, &mult, &shift);
+        if (s != QNN_OK || d.N == 0)
+            return s;
+    }
+    qnn_plan *p = nullptr;
+    qnn_status s = make_conv_plan(d, st, &p);
+    if (s != QNN_OK)
+        return s;
+    if ((s = alloc_ws(p)) == QNN_OK && (s = run_plan(p, st, x, y, nullptr)) == QNN_OK) {
+        const hipError_t e = hipStreamSynchronize(st);
+        if (e != hipSuccess)
+            s = hip_fail(e, "stream synchronize");
+    }
+    free_plan(p);
+    return s;
+}
+
+ConvDesc conv_desc(qnn_dtype xt, int32_t N, int32_t H, int32_t W, int32_t C, qnn_qparams xq, const int8_t *w,
+                   int32_t K, int32_t R, int32_t S, qnn_qparams wq, const int32_t *bias, qnn_conv_params cp,
+                   qnn_dtype yt, qnn_qparams yq, qnn_clamp act, qnn_rounding rnd, int32_t y_ldc, int32_t y_coff,
+                   bool dw)
+{
+    return ConvDesc{xt, N, H, W, C, xq, w, K, R, S, wq, bias, cp, yt, yq, act, rnd, y_ldc, y_coff, dw};
+}
+
+ConvDesc dense_desc(qnn_dtype xt, int32_t M, int32_t Kd, qnn_qparams xq, const int8_t *w, int32_t Nd,
+                    qnn_qparams wq, const int32_t *bias, qnn_dtype yt, qnn_qparams yq, qnn_clamp act,
+                    qnn_rounding rnd, int32_t y_ldc)
+{
+    // dense is the 1x1 conv of a [1][1][M][Kd] "image"
+    const qnn_conv_params cp{1, 1, 0, 0, 0, 0, 1, 1};
+    return ConvDesc{xt, M > 0 ? 1 : 0, 1, M > 0 ? M : 1, Kd, xq, w, Nd, 1, 1, wq, bias, cp, yt, yq, act, rnd,
+                    y_ldc, 0, false};
+}
+
+qnn_status make_req_plan(qnn_dtype xt, int64_t count, int32_t channels, qnn_qparams xq, qnn_dtype yt,
+                         qnn_qparams yq, qnn_clamp act, qnn_rounding rnd, hipStream_t st, bool upload,
+                         qnn_plan **out)
+{
+    if (xt != QNN_UINT8 && xt != QNN_INT8 && xt != QNN_INT32)
+        return fail(QNN_ERR_DTYPE, "requantize: unknown input dtype");
+    if (yt != QNN_UINT8 && yt != QNN_INT8 && yt != QNN_INT32)
+        return fail(QNN_ERR_DTYPE, "requantize: unknown output dtype");
+    if (rnd != QNN_ROUND_HALF_UP && rnd != QNN_ROUND_HALF_AWAY)
+        return fail(QNN_ERR_QPARAM, "requantize: unknown rounding %d", (int)rnd);
+    if (count < 0 || channels < 1 || count % channels != 0)
+        return fail(QNN_ERR_SHAPE, "requantize: count must be a non-negative multiple of channels >= 1");
+    qnn_status s;
+    if ((s = check_qparams(xq, "x qparams", channels, xt, false)) != QNN_OK)
+        return s;
+    if ((s = check_qparams(yq, "y qparams", channels, yt, false)) != QNN_OK)
+        return s;
+    if (xt == QNN_INT32)
+        for (int i = 0; i < xq.n; ++i)
+            if (xq.zero_point[i] != 0)
+                return fail(QNN_ERR_QPARAM, "requantize: int32 input requires zero point 0");
+    int32_t lo, hi;
+    if ((s = out_bounds(yt, act, &lo, &hi)) != QNN_OK)
+        return s;
+    const bool perch = xq.n > 1 || yq.n > 1;
+    const int nc = perch ? channels : 1;
+    std::vector<int32_t> tab(4 * (size_t)nc);
+    for (int c = 0; c < nc; ++c) {
+        const int ci = xq.n == 1 ? 0 : c, co = yq.n == 1 ? 0 : c;
+        const double M = (double)xq.scale[ci] / (double)yq.scale[co];
+        int32_t m, n;
+        if (!derive_multiplier(M, &m, &n))
+            return fail(QNN_ERR_QPARAM, "requantize: multiplier %g is out of range", M);
+        tab[4 * c] = m;
+        tab[4 * c + 1] = n > 63 ? 63 : n;
+        tab[4 * c + 2] = xq.zero_point[ci];
+        tab[4 * c + 3] = yq.zero_point[co];
+    }
+    qnn_plan *p = new (std::nothrow) qnn_plan();
+    if (!p)
+        return fail(QNN_ERR_ALLOC, "out of host memory");
+    p->kind = PLAN_REQ;
+    p->xdt = xt;
+    p->ydt = yt;
+    ReqArgs &a = p->req;
+    a.count = count;
+    a.channels = channels;
+    a.mult = tab[0]; a.shift = tab[1]; a.zp_in = tab[2]; a.zp_out = tab[3];
+    a.lo = lo; a.hi = hi; a.rounding = rnd;
+    a.tab = nullptr;
+    if (perch) {
+        if (!upload) {
+            free_plan(p);
+            return fail(QNN_ERR_UNSUPPORTED, "internal: per-channel requantize needs an upload");
+        }
+        hipError_t e = hipMalloc(&p->dev, tab.size() * sizeof(int32_t));
+        if (e != hipSuccess) {
+            free_plan(p);
+            return fail(QNN_ERR_ALLOC, "hipMalloc failed");
+        }
+        if ((e = hipMemcpyAsync(p->dev, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice, st)) !=
+                hipSuccess ||
+            (e = hipStreamSynchronize(st)) != hipSuccess) {
+            free_plan(p);
+            return hip_fail(e, "requantize table upload");
+        }
+        a.tab = (const int32_t *)p->dev;
+    }
+    char buf[96];
+    snprintf(buf, sizeof buf, "requantize %s->%s count=%lld channels=%d perch=%d", dtype_name(xt), dtype_name(yt),
+             (long long)count, channels, (int)perch);
+    p->desc = buf;
+    *out = p;
+    return QNN_OK;
+}
+
+}  // namespace
+
+// ==================================================================== ABI
+
+extern "C" {
+
+int32_t qnn_abi_version(void) { return QNN_ABI_VERSION; }
+
+const char *qnn_last_error(void) { return g_last_error.c_str(); }
+
+const char *qnn_status_string(qnn_status s)
+{
+    switch (s) {
+    case QNN_OK: return "QNN_OK";
+    case QNN_ERR_NULL: return "QNN_ERR_NULL";
+    case QNN_ERR_SHAPE: return "QNN_ERR_SHAPE";
+    case QNN_ERR_DTYPE: return "QNN_ERR_DTYPE";
+    case QNN_ERR_QPARAM: return "QNN_ERR_QPARAM";
+    case QNN_ERR_OVERFLOW: return "QNN_ERR_OVERFLOW";
+    case QNN_ERR_UNSUPPORTED: return "QNN_ERR_UNSUPPORTED";
+    case QNN_ERR_HIP: return "QNN_ERR_HIP";
+    case QNN_ERR_ALLOC: return "QNN_ERR_ALLOC";
+    }
+    return "QNN_ERR_?";
+}
+
+qnn_status qnn_quantize_multiplier(double M, int32_t *mult, int32_t *shift)
+{
+    if (!mult || !shift)
+        return fail(QNN_ERR_NULL, "quantize_multiplier: NULL output pointer");
+    if (!derive_multiplier(M, mult, shift))
+        return fail(QNN_ERR_QPARAM, "multiplier %g is negative, not finite or too large", M);
+    return QNN_OK;
+}
+
+qnn_status qnn_conv2d(void *stream, const void *x, qnn_dtype x_dtype, int32_t N, int32_t H, int32_t W, int32_t C,
+                      qnn_qparams x_q, const int8_t *w, int32_t K, int32_t R, int32_t S, qnn_qparams w_q,
+                      const int32_t *bias, qnn_conv_params conv, void *y, qnn_dtype y_dtype, qnn_qparams y_q,
+                      qnn_clamp act, qnn_rounding rounding, int32_t y_ldc, int32_t y_coff)
+{
+    const ConvDesc d = conv_desc(x_dtype, N, H, W, C, x_q, w, K, R, S, w_q, bias, conv, y_dtype, y_q, act,
+                                 rounding, y_ldc, y_coff, false);
+    if (N > 0 && (!x || !y))
+        return fail(QNN_ERR_NULL, "conv2d: x or y is NULL");
+    return one_shot(d, (hipStream_t)stream, x, y);
+}
+
+qnn_status qnn_depthwise_conv2d(void *stream, const void *x, qnn_dtype x_dtype, int32_t N, int32_t H, int32_t W,
+                                int32_t C, qnn_qparams x_q, const int8_t *w, int32_t R, int32_t S, qnn_qparams w_q,
+                                const int32_t *bias, qnn_conv_params conv, void *y, qnn_dtype y_dtype,
+                                qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding, int32_t y_ldc,
+                                int32_t y_coff)
+{
+    const ConvDesc d = conv_desc(x_dtype, N, H, W, C, x_q, w, C, R, S, w_q, bias, conv, y_dtype, y_q, act,
+                                 rounding, y_ldc, y_coff, true);
+    if (N > 0 && (!x || !y))
+        return fail(QNN_ERR_NULL, "depthwise_conv2d: x or y is NULL");
+    return one_shot(d, (hipStream_t)stream, x, y);
+}
+
+qnn_status qnn_dense(void *stream, const void *x, qnn_dtype x_dtype, int32_t M, int32_t Kd, qnn_qparams x_q,
+                     const int8_t *w, int32_t Nd, qnn_qparams w_q, const int32_t *bias, void *y, qnn_dtype y_dtype,
+                     qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding, int32_t y_ldc)
+{
+    if (M < 0)
+        return fail(QNN_ERR_SHAPE, "dense: M must be >= 0");
+    const ConvDesc d = dense_desc(x_dtype, M, Kd, x_q, w, Nd, w_q, bias, y_dtype, y_q, act, rounding, y_ldc);
+    if (M > 0 && (!x || !y))
+        return fail(QNN_ERR_NULL, "dense: x or y is NULL");
+    return one_shot(d, (hipStream_t)stream, x, y);
+}
+
+qnn_status qnn_requantize(void *stream, const void *x, qnn_dtype x_dtype, int64_t count, int32_t channels,
+                          qnn_qparams x_q, void *y, qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act,
+                          qnn_rounding rounding)
+{
+    hipStream_t st = (hipStream_t)stream;
+    qnn_plan *p = nullptr;
+    qnn_status s = make_req_plan(x_dtype, count, channels, x_q, y_dtype, y_q, act, rounding, st, true, &p);
+    if (s != QNN_OK)
+        return s;
+    if (count > 0 && (!x || !y)) {
+        free_plan(p);
+        return fail(QNN_ERR_NULL, "requantize: x or y is NULL");
+    }
+    s = run_plan(p, st, x, y, nullptr);
+    if (s == QNN_OK && p->dev) {
+        const hipError_t e = hipStreamSynchronize(st);
+        if (e != hipSuccess)
+            s = hip_fail(e, "stream synchronize");
+    }
+    free_plan(p);
+    return s;
+}
+
+qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a_q, const void *b,
+                   qnn_dtype b_dtype, qnn_qparams b_q, int64_t count, void *y, qnn_dtype y_dtype,
+                   qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding)
+{
+    if (a_dtype != QNN_UINT8 && a_dtype != QNN_INT8)
+        return fail(QNN_ERR_DTYPE, "add: a must be uint8 or int8");
+    if (b_dtype != QNN_UINT8 && b_dtype != QNN_INT8)
+        return fail(QNN_ERR_DTYPE, "add: b must be uint8 or int8");
+    if (y_dtype != QNN_UINT8 && y_dtype != QNN_INT8)
+        return fail(QNN_ERR_DTYPE, "add: y must be uint8 or int8");
+    if (rounding != QNN_ROUND_HALF_UP && rounding != QNN_ROUND_HALF_AWAY)
+        return fail(QNN_ERR_QPARAM, "add: unknown rounding %d", (int)rounding);
+    if (count < 0)
+        return fail(QNN_ERR_SHAPE, "add: count must be >= 0");
+    qnn_status s;
+    if ((s = check_qparams(a_q, "a qparams", 1, a_dtype, false)) != QNN_OK ||
+        (s = check_qparams(b_q, "b qparams", 1, b_dtype, false)) != QNN_OK ||
+        (s = check_qparams(y_q, "y qparams", 1, y_dtype, false)) != QNN_OK)
+        return s;
+    AddArgs args{};
+    if ((s = out_bounds(y_dtype, act, &args.lo, &args.hi)) != QNN_OK)
+        return s;
+    const double Ma = (double)a_q.scale[0] / (double)y_q.scale[0];
+    const double Mb = (double)b_q.scale[0] / (double)y_q.scale[0];
+    if (!derive_multiplier(Ma, &args.ma, &args.na) || !derive_multiplier(Mb, &args.mb, &args.nb))
+        return fail(QNN_ERR_QPARAM, "add: multiplier out of range (%g, %g)", Ma, Mb);
+    args.na = std::min(args.na, 63);
+    args.nb = std::min(args.nb, 63);
+    if (count == 0)
+        return QNN_OK;
+    if (!a || !b || !y)
+        return fail(QNN_ERR_NULL, "add: a, b or y is NULL");
+    args.a = a;
+    args.b = b;
+    args.y = y;
+    args.count = count;
+    args.zpa = a_q.zero_point[0];
+    args.zpb = b_q.zero_point[0];
+    args.zp_y = y_q.zero_point[0];
+    args.rounding = rounding;
+    const bool aligned = (((uintptr_t)a | (uintptr_t)b | (uintptr_t)y) & 15) == 0;
+    const hipError_t e = launch_add(args, a_dtype, b_dtype, y_dtype, aligned, (hipStream_t)stream);
+    return e == hipSuccess ? QNN_OK : hip_fail(e, "add launch");
+}
+
+qnn_status qnn_conv2d_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t N, int32_t H,
+                                  int32_t W, int32_t C, qnn_qparams x_q, const int8_t *w, int32_t K, int32_t R,
+                                  int32_t S, qnn_qparams w_q, const int32_t *bias, qnn_conv_params conv,
+                                  qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding,
+                                  int32_t y_ldc, int32_t y_coff)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    const ConvDesc d = conv_desc(x_dtype, N, H, W, C, x_q, w, K, R, S, w_q, bias, conv, y_dtype, y_q, act,
+                                 rounding, y_ldc, y_coff, false);
+    qnn_plan *p = nullptr;
+    qnn_status s = make_conv_plan(d, (hipStream_t)stream, &p);
+    if (s == QNN_OK && (s = alloc_ws(p)) != QNN_OK) {
+        free_plan(p);
+        return s;
+    }
+    *plan = p;
+    return s;
+}
+
+qnn_status qnn_depthwise_conv2d_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t N, int32_t H,
+                                            int32_t W, int32_t C, qnn_qparams x_q, const int8_t *w, int32_t R,
+                                            int32_t S, qnn_qparams w_q, const int32_t *bias, qnn_conv_params conv,
+                                            qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act,
+                                            qnn_rounding rounding, int32_t y_ldc, int32_t y_coff)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    const ConvDesc d = conv_desc(x_dtype, N, H, W, C, x_q, w, C, R, S, w_q, bias, conv, y_dtype, y_q, act,
+                                 rounding, y_ldc, y_coff, true);
+    return make_conv_plan(d, (hipStream_t)stream, plan);
+}
+
+qnn_status qnn_dense_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t M, int32_t Kd,
+                                 qnn_qparams x_q, const int8_t *w, int32_t Nd, qnn_qparams w_q, const int32_t *bias,
+                                 qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding,
+                                 int32_t y_ldc)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    if (M < 0)
+        return fail(QNN_ERR_SHAPE, "dense: M must be >= 0");
+    const ConvDesc d = dense_desc(x_dtype, M, Kd, x_q, w, Nd, w_q, bias, y_dtype, y_q, act, rounding, y_ldc);
+    qnn_plan *p = nullptr;
+    qnn_status s = make_conv_plan(d, (hipStream_t)stream, &p);
+    if (s == QNN_OK && (s = alloc_ws(p)) != QNN_OK) {
+        free_plan(p);
+        return s;
+    }
+    *plan = p;
+    return s;
+}
+
+qnn_status qnn_requantize_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int64_t count,
+                                      int32_t channels, qnn_qparams x_q, qnn_dtype y_dtype, qnn_qparams y_q,
+                                      qnn_clamp act, qnn_rounding rounding)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    return make_req_plan(x_dtype, count, channels, x_q, y_dtype, y_q, act, rounding, (hipStream_t)stream, true,
+                         plan);
+}
+
+qnn_status qnn_plan_run(const qnn_plan *plan, void *stream, const void *x, void *y, void *workspace)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_run: plan is NULL");
+    return run_plan(plan, (hipStream_t)stream, x, y, workspace);
+}
+
+size_t qnn_plan_workspace_size(const qnn_plan *plan) { return plan ? plan->ws_bytes : 0; }
+
+const char *qnn_plan_describe(const qnn_plan *plan) { return plan ? plan->desc.c_str() : ""; }
+
+void qnn_plan_destroy(qnn_plan *plan) { free_plan(plan); }
+
+}  // extern "C"

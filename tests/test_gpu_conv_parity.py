@@ -1,0 +1,280 @@
+"""GPU parity of conv2d / dense / depthwise + requantize: the HIP path (called
+through the C ABI) against the CPU oracle, element by element, bit-exact."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # the gpu marker deselects these on CPU hosts
+    pytest.skip("no GPU", allow_module_level=True)
+
+from gpu_util import (Q, O, log, dev, env, run_gpu, run_oracle, oracle_points, make_plan, assert_equal)  # noqa: E402
+
+
+@pytest.mark.parametrize("s_y", [0.05, 0.5], ids=["sy0.05", "sy0.5"])
+@pytest.mark.parametrize("one_shot", [False, True], ids=["plan", "oneshot"])
+def test_single_conv_14x14x64(s_y, one_shot):
+    c = W.single_conv_case(seed=1, s_y=s_y)
+    log(f"single conv s_y={s_y} one_shot={one_shot}")
+    assert_equal(run_gpu(c, one_shot), run_oracle(c), "conv14x14x64")
+
+
+@pytest.mark.parametrize("layer,seed", [(W.bert_ffn()[0], 2), (W.bert_ffn()[1], 3)], ids=["768to3072", "3072to768"])
+def test_dense_bert_ffn(layer, seed):
+    c = W.dense_case(layer, seed)
+    log(f"dense {layer}")
+    assert_equal(run_gpu(c), run_oracle(c), layer.name)
+    assert_equal(run_gpu(c, one_shot=True), run_oracle(c), layer.name + " one-shot")
+
+
+def test_resnet50_batch1_full():
+    for i, layer in enumerate(W.resnet50()):
+        c = W.conv_case(layer, 1, seed=3000 + i)
+        log(f"resnet50 b1 {layer.name}")
+        assert_equal(run_gpu(c), run_oracle(c), layer.name)
+
+
+def test_resnet50_batch32_sampled():
+    """The benchmark configuration (batch 32, the plans bench.py times),
+    checked on sampled outputs."""
+    for i, layer in enumerate(W.resnet50()):
+        c = W.conv_case(layer, 32, seed=3000 + i)
+        log(f"resnet50 b32 {layer.name}")
+        p, keep = make_plan(c)
+        y = p.run(dev(c.x)).cpu().numpy()
+        p.close()
+        idx = W.sample_indices(y.size, 3000, seed=i)
+        assert_equal(y.reshape(-1)[idx], oracle_points(c, idx), layer.name)
+
+
+def _mobilenet_cases(N):
+    out = []
+    for i, layer in enumerate(W.mobilenet_v2_layers()):
+        if isinstance(layer, W.AddLayer):
+            out.append(("add", layer, W.add_case(layer, N, seed=4000 + i)))
+        else:
+            out.append(("conv", layer, W.conv_case(layer, N, seed=4000 + i)))
+    return out
+
+
+def _check_add(case, sample=None):
+    a, b = dev(case.a), dev(case.b)
+    y = Q.add(a, case.s_a, case.zp_a, b, case.s_b, case.zp_b, case.s_o, case.zp_o, case.yt, case.act,
+              case.rounding).cpu().numpy()
+    ref = O.add(case.a, case.s_a, case.zp_a, case.b, case.s_b, case.zp_b, case.s_o, case.zp_o, case.yt, case.act,
+                case.rounding)
+    assert_equal(y, ref, case.name)
+
+
+def test_mobilenet_v2_batch1_full():
+    for kind, layer, c in _mobilenet_cases(1):
+        log(f"mobilenet b1 {layer.name}")
+        if kind == "add":
+            _check_add(c)
+        else:
+            assert_equal(run_gpu(c), run_oracle(c), layer.name)
+
+
+def test_mobilenet_v2_batch64_sampled():
+    for kind, layer, c in _mobilenet_cases(64):
+        log(f"mobilenet b64 {layer.name}")
+        if kind == "add":
+            _check_add(c)
+            continue
+        p, keep = make_plan(c)
+        y = p.run(dev(c.x)).cpu().numpy()
+        p.close()
+        idx = W.sample_indices(y.size, 3000, seed=7)
+        assert_equal(y.reshape(-1)[idx], oracle_points(c, idx), layer.name)
+
+
+def _inception_groups():
+    """Per concat group: the common output (s, zp) and the member layers."""
+    groups = {}
+    for i, layer in enumerate(W.inception_v3()):
+        if layer.concat:
+            groups.setdefault(layer.concat[0], []).append((i, layer))
+    return groups
+
+
+@pytest.mark.parametrize("N", [1, 64], ids=["b1_full", "b64_sampled"])
+def test_inception_v3_concat_blocks(N):
+    """Every branch writes its channel slice of the block output with the
+    block's common (scale, zero point); channels no conv writes (the pooling
+    branches) keep their sentinel value."""
+    rng = np.random.default_rng(5)
+    for g, members in _inception_groups().items():
+        total = members[0][1].concat[2]
+        s_y = float(np.float32(10 ** rng.uniform(-1.5, -0.5)))
+        zp_y = int(rng.integers(0, 256))
+        Ho = Wo = None
+        cases = []
+        for i, layer in members:
+            c = W.conv_case(layer, N, seed=5000 + i, out_q=(s_y, zp_y))
+            cases.append((i, layer, c))
+        # output spatial size from the first member
+        ho, wo = Q.out_hw(members[0][1].H, members[0][1].W, members[0][1].R, members[0][1].S,
+                          members[0][1].stride, members[0][1].pads)
+        out = torch.full((N, ho, wo, total), 77, dtype=torch.uint8, device="cuda")
+        written = np.zeros(total, bool)
+        refs = []
+        for i, layer, c in cases:
+            log(f"inception b{N} {layer.name} -> {g}[{layer.concat[1]}:+{layer.Cout}]")
+            p, keep = make_plan(c, y_ldc=total, y_coff=layer.concat[1])
+            p.run(dev(c.x), out=out)
+            torch.cuda.synchronize()
+            p.close()
+            written[layer.concat[1]:layer.concat[1] + layer.Cout] = True
+            refs.append((layer, c))
+        y = out.cpu().numpy()
+        assert (y[..., ~written] == 77).all(), g
+        for layer, c in refs:
+            sl = y[..., layer.concat[1]:layer.concat[1] + layer.Cout]
+            if N == 1:
+                assert_equal(sl, run_oracle(c), layer.name)
+            else:
+                flat = np.ascontiguousarray(sl).reshape(-1)
+                idx = W.sample_indices(flat.size, 2000, seed=9)
+                assert_equal(flat[idx], oracle_points(c, idx), layer.name)
+
+
+def test_inception_v3_other_layers_batch1():
+    for i, layer in enumerate(W.inception_v3()):
+        if layer.concat:
+            continue
+        c = W.conv_case(layer, 1, seed=5000 + i)
+        log(f"inception b1 {layer.name}")
+        assert_equal(run_gpu(c), run_oracle(c), layer.name)
+
+
+# ------------------------------------------------------------------ variants
+
+VARIANTS = [
+    # (name, layer, N, kwargs)
+    ("zpw_tensor", W.ConvLayer("v", 9, 11, 32, 40, 3, 3, 1, (1, 1, 1, 1)), 2, dict(zp_w="tensor")),
+    ("zpw_channel", W.ConvLayer("v", 13, 7, 48, 24, 3, 3, 2, (1, 0, 1, 2)), 3, dict(zp_w="channel")),
+    ("zpw_channel_1x1", W.ConvLayer("v", 5, 5, 64, 100, 1, 1), 4, dict(zp_w="channel")),
+    ("half_away", W.ConvLayer("v", 10, 10, 64, 64, 3, 3, 1, (1, 1, 1, 1)), 2, dict(rounding="half_away")),
+    ("int8_x", W.ConvLayer("v", 10, 12, 32, 48, 3, 3, 1, (1, 1, 1, 1)), 2, dict(x_dtype="i8")),
+    ("int8_y", W.ConvLayer("v", 10, 12, 32, 48, 3, 3, 1, (1, 1, 1, 1)), 2, dict(yt="i8")),
+    ("int32_y", W.ConvLayer("v", 10, 12, 32, 48, 3, 3, 1, (1, 1, 1, 1)), 2, dict(yt="i32")),
+    ("int32_y_zpw", W.ConvLayer("v", 8, 9, 16, 20, 3, 3, 2, (0, 1, 2, 0)), 2, dict(yt="i32", zp_w="channel")),
+    ("no_bias_no_act", W.ConvLayer("v", 7, 7, 128, 130, 3, 3, 1, (1, 1, 1, 1)), 1, dict(bias=False, act=None)),
+    ("ragged_cout", W.ConvLayer("v", 6, 6, 32, 37, 3, 3, 1, (1, 1, 1, 1)), 3, {}),
+    ("cin3_stem", W.ConvLayer("v", 31, 29, 3, 64, 7, 7, 2, (3, 3, 3, 3)), 2, {}),
+    ("cin24_1x1", W.ConvLayer("v", 14, 14, 24, 144, 1, 1), 2, {}),
+    ("cin20", W.ConvLayer("v", 9, 9, 20, 36, 3, 3, 1, (1, 1, 1, 1)), 2, {}),
+    ("cin5", W.ConvLayer("v", 9, 9, 5, 8, 3, 3, 1, (2, 2, 2, 2)), 2, dict(zp_w="channel")),
+    ("one_pixel", W.ConvLayer("v", 1, 1, 64, 64, 1, 1), 1, {}),
+    ("big_filter", W.ConvLayer("v", 7, 7, 32, 16, 7, 7, 1, (3, 3, 3, 3)), 1, {}),
+    ("1x7", W.ConvLayer("v", 17, 17, 128, 128, 1, 7, 1, (0, 3, 0, 3)), 2, {}),
+    ("7x1", W.ConvLayer("v", 17, 17, 128, 192, 7, 1, 1, (3, 0, 3, 0)), 2, {}),
+    ("stride2_asym", W.ConvLayer("v", 16, 15, 64, 64, 3, 3, 2, (0, 0, 1, 1)), 2, {}),
+    ("deep_J", W.ConvLayer("v", 7, 7, 512, 64, 3, 3, 1, (1, 1, 1, 1)), 2, {}),
+    ("dw_zpw", W.ConvLayer("v", 12, 12, 32, 32, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, dict(zp_w="channel")),
+    ("dw_s2_i8", W.ConvLayer("v", 13, 13, 24, 24, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2, dict(x_dtype="i8")),
+    ("dw_odd_c", W.ConvLayer("v", 9, 9, 7, 7, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, {}),
+    ("dw_5x5_i32", W.ConvLayer("v", 9, 9, 16, 16, 5, 5, 1, (2, 2, 2, 2), depthwise=True), 2, dict(yt="i32")),
+    ("dw_half_away", W.ConvLayer("v", 8, 8, 64, 64, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2,
+     dict(rounding="half_away")),
+]
+
+
+@pytest.mark.parametrize("name,layer,N,kw", VARIANTS, ids=[v[0] for v in VARIANTS])
+def test_conv_variants(name, layer, N, kw):
+    c = W.conv_case(layer, N, seed=zlib.crc32(name.encode()) % 1000, **kw)
+    log(f"variant {name}")
+    assert_equal(run_gpu(c), run_oracle(c), name)
+
+
+@pytest.mark.parametrize("tile", [0, 1, 2, 3])
+@pytest.mark.parametrize("split", [1, 3])
+def test_every_tile_and_split(tile, split):
+    """Each kernel instantiation (tile shape x split-K), forced, on ragged
+    shapes that span several tiles."""
+    layer = W.ConvLayer("t", 23, 21, 64, 200, 3, 3, 1, (1, 1, 1, 1))
+    with env(QNN_TILE=tile, QNN_SPLIT=split):
+        for kw in ({}, dict(zp_w="channel"), dict(yt="i32")):
+            c = W.conv_case(layer, 2, seed=tile * 10 + split, **kw)
+            assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} split {split} {kw}")
+        c = W.conv_case(W.ConvLayer("t", 9, 9, 3, 70, 5, 5, 2, (2, 2, 2, 2)), 3, seed=1)
+        assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} split {split} narrow gather")
+
+
+def test_random_shapes():
+    rng = np.random.default_rng(123)
+    for t in range(40):
+        R, S = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        H, Wd = int(rng.integers(R, 20)), int(rng.integers(S, 20))
+        C = int(rng.choice([1, 3, 4, 8, 16, 32, 48, 64, 96, 160, 256]))
+        K = int(rng.integers(1, 300))
+        st = int(rng.integers(1, 3))
+        pads = tuple(int(v) for v in rng.integers(0, 3, size=4))
+        layer = W.ConvLayer("r", H, Wd, C, K, R, S, st, pads)
+        kw = dict(zp_w=str(rng.choice(["zero", "tensor", "channel"])),
+                  rounding=str(rng.choice(["half_up", "half_away"])),
+                  x_dtype=str(rng.choice(["u8", "i8"])), yt=str(rng.choice(["u8", "i8", "i32"])),
+                  bias=bool(rng.integers(0, 2)))
+        c = W.conv_case(layer, int(rng.integers(1, 4)), seed=t, **kw)
+        log(f"random {t}: {layer} {kw}")
+        assert_equal(run_gpu(c), run_oracle(c), f"random {t}")
+
+
+def test_empty_batch_is_noop():
+    c = W.single_conv_case()
+    x = torch.empty((0, 14, 14, 64), dtype=torch.uint8, device="cuda")
+    y = Q.conv2d(x, c.s_x, c.zp_x, dev(c.w), c.s_w, c.zp_w, None, 1, 1, 1, c.s_y, c.zp_y, "u8")
+    assert y.shape == (0, 14, 14, 64)
+    p, keep = make_plan(c, N=0)
+    p.run(x)
+    torch.cuda.synchronize()
+    p.close()
+
+
+def test_plan_workspace_and_streams():
+    """Two runs of one split-K plan on two streams, each with its own
+    workspace, give the oracle's result."""
+    layer = W.ConvLayer("ws", 7, 7, 512, 512, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 2, seed=11, zp_w="channel")
+    ref = run_oracle(c)
+    with env(QNN_SPLIT=4):
+        p, keep = make_plan(c)
+    assert p.workspace_size > 0, p.describe()
+    x = dev(c.x)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    ws1 = torch.empty(p.workspace_size, dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty(p.workspace_size, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        y1 = p.run(x, workspace=ws1, stream=s1)
+    with torch.cuda.stream(s2):
+        y2 = p.run(x, workspace=ws2, stream=s2)
+    torch.cuda.synchronize()
+    assert_equal(y1.cpu().numpy(), ref, "stream 1")
+    assert_equal(y2.cpu().numpy(), ref, "stream 2")
+    p.close()
+
+
+def test_accumulator_near_int32_bound():
+    """Extreme values at the accumulator bound: all-255 activations with zero
+    point 0, all -128 weights with zero point 127, J = 33000 taps, so the
+    true accumulator is -255*255*J = -2145825000, just inside int32, while
+    the folded terms of Eq. (3) individually stay in range only modulo 2^32."""
+    layer = W.ConvLayer("ext", 2, 2, 33000, 8, 1, 1)
+    c = W.conv_case(layer, 1, seed=1, yt="i32", bias=False, zp_w="tensor")
+    c.x[:] = 255
+    c.zp_x = 0
+    c.w[:] = -128
+    c.zp_w[:] = 127
+    ref = run_oracle(c)
+    assert int(ref.min()) == -255 * 255 * 33000
+    assert_equal(run_gpu(c), ref, "extreme int32")
+    c.yt = "u8"
+    c.act = None
+    c.s_y = 1.0
+    assert_equal(run_gpu(c), run_oracle(c), "extreme u8")
