@@ -137,7 +137,7 @@ def kernel_group(it):
     if it.kind == "dw":
         return "depthwise"
     d = dict(kv.split("=") for kv in it.desc.split()[1:] if "=" in kv)
-    return f"conv_mfma tile={d['tile']} gather={d['gather']} split={'1' if d['split'] == '1' else 'k'}"
+    return f"conv_mfma tile={d['tile']} gather={d['gather']}"
 
 
 # ------------------------------------------------------------------ timing

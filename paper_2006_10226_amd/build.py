@@ -18,6 +18,8 @@ FLAGS = [
     "-I" + INCLUDE, "-I" + CSRC,
     # no packed-fp32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep per-thread register arrays in registers (never staged through LDS)
+    "-mllvm", "-disable-promote-alloca-to-lds",
 ]
 
 

@@ -93,22 +93,22 @@ __global__ void __launch_bounds__(256) depthwise_kernel(DwArgs a)
 
 // wq[t][c] = w[t][c] - zp_w[c]; chan[c].bconst = bias[c].
 __global__ void __launch_bounds__(256) prep_dw_kernel(const int8_t *w, const int32_t *bias, int RS, int C,
-                                                      int32_t *wq, ChanRec *chan)
+                                                      const int32_t *zpw, int32_t *wq, ChanRec *chan)
 {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= RS * C)
         return;
     const int c = i % C;
-    wq[i] = (int)w[i] - chan[c].zpw;
+    wq[i] = (int)w[i] - zpw[c];
     if (i < C)
         chan[c].bconst = bias ? bias[c] : 0;
 }
 
-hipError_t launch_prep_dw(const int8_t *w, const int32_t *bias, int RS, int C, int32_t *wq, ChanRec *chan,
-                          hipStream_t st)
+hipError_t launch_prep_dw(const int8_t *w, const int32_t *bias, int RS, int C, const int32_t *zpw, int32_t *wq,
+                          ChanRec *chan, hipStream_t st)
 {
     const int n = RS * C;
-    hipLaunchKernelGGL(prep_dw_kernel, dim3((n + 255) / 256), dim3(256), 0, st, w, bias, RS, C, wq, chan);
+    hipLaunchKernelGGL(prep_dw_kernel, dim3((n + 255) / 256), dim3(256), 0, st, w, bias, RS, C, zpw, wq, chan);
     return hipGetLastError();
 }
 

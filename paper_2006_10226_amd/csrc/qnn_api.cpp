@@ -142,7 +142,9 @@ struct qnn_plan {
     ConvArgs conv{};
     int tile = 0, avec = 16, mode = OUT_REQUANT;
     bool term3 = false;
-    size_t ws_partial_bytes = 0, ws_asum_bytes = 0;
+    size_t ws_asum_bytes = 0, ws_xpad_bytes = 0;
+    int32_t C_in = 0;           // channels of the caller's x (before padding to a.C)
+    uint8_t pad_zp = 0;         // zero point byte written into padded channels
     // depthwise
     DwArgs dw{};
     // requantize
@@ -279,42 +281,30 @@ qnn_status read_bias(const int32_t *bias, int n, hipStream_t st, std::vector<int
     return QNN_OK;
 }
 
-// Tile and split-K choice for an implicit-GEMM problem of M pixels x K
-// channels x J reduction.
-void choose_tiling(int64_t M, int K, int J, int *tile, int *nsplit, int *ksteps, int *tiles_c, int *nblocks,
-                   int *Kpad, int *Jpad)
+// Tile choice for an implicit-GEMM problem of M pixels x K channels x J
+// reduction (QNN_TILE overrides it for sweeps).
+int choose_tile(int64_t M, int K, int J)
 {
-    int t = env_int("QNN_TILE", -1);
-    if (t < 0 || t >= TILE_COUNT) {
-        const int64_t big = (M + 127) / 128 * ((K + 127) / 128);
-        if (big < 160)
-            t = TILE_64x64;
-        else if (K <= 64)
-            t = TILE_64x256;
+    const int t = env_int("QNN_TILE", -1);
+    if (t >= 0 && t < TILE_COUNT)
+        return t;
+    (void)M;
+    (void)K;
+    return J <= 64 ? TILE_64x64_K64 : TILE_64x64;
+}
+
+int device_cus()
+{
+    static int cus = 0;
+    if (!cus) {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+            cus = n;
         else
-            t = TILE_128x128;
+            cus = 256;
     }
-    const TileShape ts = tile_shape(t);
-    *tile = t;
-    *Kpad = (int)align_up(K, ts.tc);
-    *Jpad = (int)align_up(J, ts.bk);
-    *tiles_c = *Kpad / ts.tc;
-    const int64_t tiles_p = (M + ts.tp - 1) / ts.tp;
-    *nblocks = (int)(*tiles_c * tiles_p);
-    const int nk = *Jpad / ts.bk;
-    int ns = env_int("QNN_SPLIT", 0);
-    if (ns <= 0) {
-        ns = 1;
-        if (*nblocks > 0 && *nblocks < 256 && nk >= 4) {
-            ns = (int)((512 + *nblocks - 1) / *nblocks);
-            ns = std::min(ns, nk / 2);
-            ns = std::min(ns, 16);
-            ns = std::max(ns, 1);
-        }
-    }
-    ns = std::min(ns, nk);
-    *ksteps = (nk + ns - 1) / ns;
-    *nsplit = (nk + *ksteps - 1) / *ksteps;
+    return cus;
 }
 
 qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
@@ -341,19 +331,25 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         p->kind = PLAN_DW;
         const int C = d.C, RS = d.R * d.S;
         const size_t wq_bytes = align_up(sizeof(int32_t) * RS * C, 256);
-        const size_t ch_bytes = sizeof(ChanRec) * C;
-        hipError_t e = hipMalloc(&p->dev, wq_bytes + ch_bytes);
+        const size_t ch_bytes = align_up(sizeof(ChanRec) * C, 256);
+        const size_t zw_bytes = align_up(sizeof(int32_t) * C, 256);
+        hipError_t e = hipMalloc(&p->dev, wq_bytes + ch_bytes + zw_bytes);
         if (e != hipSuccess) {
             free_plan(p);
-            return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", wq_bytes + ch_bytes);
+            return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", wq_bytes + ch_bytes + zw_bytes);
         }
         int32_t *wq = (int32_t *)p->dev;
         ChanRec *chan = (ChanRec *)((char *)p->dev + wq_bytes);
-        std::vector<ChanRec> ch(C);
-        for (int c = 0; c < C; ++c)
-            ch[c] = ChanRec{mult[c], shift[c], 0, d.wq.zero_point[d.wq.n == 1 ? 0 : c]};
-        if ((e = hipMemcpyAsync(chan, ch.data(), ch_bytes, hipMemcpyHostToDevice, st)) != hipSuccess ||
-            (e = launch_prep_dw(d.w, d.bias, RS, C, wq, chan, st)) != hipSuccess ||
+        int32_t *zpw_d = (int32_t *)((char *)p->dev + wq_bytes + ch_bytes);
+        std::vector<uint8_t> host(ch_bytes + zw_bytes, 0);
+        for (int c = 0; c < C; ++c) {
+            const ChanRec r{mult[c], 0, 0, shift[c]};
+            const int32_t z = d.wq.zero_point[d.wq.n == 1 ? 0 : c];
+            std::memcpy(host.data() + sizeof(ChanRec) * c, &r, sizeof r);
+            std::memcpy(host.data() + ch_bytes + sizeof(int32_t) * c, &z, sizeof z);
+        }
+        if ((e = hipMemcpyAsync(chan, host.data(), host.size(), hipMemcpyHostToDevice, st)) != hipSuccess ||
+            (e = launch_prep_dw(d.w, d.bias, RS, C, zpw_d, wq, chan, st)) != hipSuccess ||
             (e = hipStreamSynchronize(st)) != hipSuccess) {
             free_plan(p);
             return hip_fail(e, "depthwise plan preparation");
@@ -379,8 +375,18 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     }
 
     p->kind = PLAN_CONV;
-    int tile, nsplit, ksteps, tiles_c, nblocks, Kpad, Jpad;
-    choose_tiling(M, d.K, (int)J, &tile, &nsplit, &ksteps, &tiles_c, &nblocks, &Kpad, &Jpad);
+    // channel counts that are not a multiple of 4 are padded (with zp_x) to C4
+    const int C4 = (d.C + 3) / 4 * 4;
+    const int RS = d.R * d.S;
+    const int64_t Jg = (int64_t)RS * C4;   // GEMM reduction length
+    const int tile = choose_tile(M, d.K, (int)Jg);
+    const TileShape ts = tile_shape(tile);
+    const int Kpad = (int)align_up(d.K, ts.tc);
+    const int Jpad = (int)align_up(Jg, ts.bk);
+    const int tiles_c = Kpad / ts.tc;
+    const int64_t ntiles = tiles_c * ((M + ts.tp - 1) / ts.tp);
+    if (ntiles >= (int64_t(1) << 31))
+        return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
     const bool term3 = [&] {
         for (int i = 0; i < d.wq.n; ++i)
             if (d.wq.zero_point[i] != 0)
@@ -389,20 +395,50 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     }();
     // legalisation (Sec. III-C): uint8 activations become int8 by x - 128
     const int32_t zpx_l = d.xt == QNN_UINT8 ? zpx - 128 : zpx;
+    // 32-bit requantize in the epilogue when every channel allows it
+    const int32_t zpy = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
+    const int32_t off8 = d.yt == QNN_INT8 ? 128 : 0;
+    bool fast = d.yt != QNN_INT32 && d.rnd == QNN_ROUND_HALF_UP;
+    for (int k = 0; k < d.K; ++k)
+        if (shift[k] < 33 || shift[k] > 53)
+            fast = false;
+
     const size_t wp_bytes = align_up((size_t)Kpad * Jpad, 256);
-    const size_t ch_bytes = sizeof(ChanRec) * Kpad;
-    hipError_t e = hipMalloc(&p->dev, wp_bytes + ch_bytes);
+    const size_t ch_bytes = align_up(sizeof(ChanRec) * Kpad, 256);
+    const size_t zw_bytes = align_up(sizeof(int32_t) * Kpad, 256);
+    const size_t pad_bytes = 256;
+    const size_t total = wp_bytes + ch_bytes + zw_bytes + pad_bytes;
+    hipError_t e = hipMalloc(&p->dev, total);
     if (e != hipSuccess) {
         free_plan(p);
-        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", wp_bytes + ch_bytes);
+        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", total);
     }
     int8_t *wp = (int8_t *)p->dev;
     ChanRec *chan = (ChanRec *)((char *)p->dev + wp_bytes);
-    std::vector<ChanRec> ch(Kpad, ChanRec{0, 1, 0, 0});
-    for (int k = 0; k < d.K; ++k)
-        ch[k] = ChanRec{mult[k], shift[k], 0, d.wq.zero_point[d.wq.n == 1 ? 0 : k]};
-    if ((e = hipMemcpyAsync(chan, ch.data(), ch_bytes, hipMemcpyHostToDevice, st)) != hipSuccess ||
-        (e = launch_prep_conv(d.w, d.bias, d.K, (int)J, Jpad, Kpad, zpx_l, wp, chan, st)) != hipSuccess ||
+    int32_t *zpw_d = (int32_t *)((char *)p->dev + wp_bytes + ch_bytes);
+    uint8_t *padbuf = (uint8_t *)p->dev + wp_bytes + ch_bytes + zw_bytes;
+    // channel records, weight zero points and the padding block (zp_x
+    // bytes) in one upload
+    std::vector<uint8_t> host(ch_bytes + zw_bytes + pad_bytes, 0);
+    for (int k = 0; k < Kpad; ++k) {
+        ChanRec r{0, 0, 0, 33};
+        int32_t z = 0;
+        if (k < d.K) {
+            r.mult = mult[k];
+            r.shift = shift[k];
+            if (fast) {
+                const int sh = shift[k] - 32;
+                r.rndzp = (int32_t)((1LL << (sh - 1)) + (int64_t)(zpy + off8) * (1LL << sh));
+            }
+            z = d.wq.zero_point[d.wq.n == 1 ? 0 : k];
+        }
+        std::memcpy(host.data() + sizeof(ChanRec) * k, &r, sizeof r);
+        std::memcpy(host.data() + ch_bytes + sizeof(int32_t) * k, &z, sizeof z);
+    }
+    std::memset(host.data() + ch_bytes + zw_bytes, (uint8_t)zpx, pad_bytes);
+    if ((e = hipMemcpyAsync(chan, host.data(), host.size(), hipMemcpyHostToDevice, st)) != hipSuccess ||
+        (e = launch_prep_conv(d.w, d.bias, d.K, RS, d.C, C4, Jpad, Kpad, zpx_l, wp, chan, zpw_d, st)) !=
+            hipSuccess ||
         (e = hipStreamSynchronize(st)) != hipSuccess) {
         free_plan(p);
         return hip_fail(e, "conv plan preparation");
@@ -411,34 +447,48 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     ConvArgs &a = p->conv;
     a.wp = wp;
     a.chan = chan;
-    a.N = d.N; a.H = d.H; a.W = d.W; a.C = d.C; a.Ho = Ho; a.Wo = Wo; a.R = d.R; a.S = d.S;
+    a.zpw = zpw_d;
+    a.padbuf = padbuf;
+    a.N = d.N; a.H = d.H; a.W = d.W; a.C = C4; a.Ho = Ho; a.Wo = Wo; a.R = d.R; a.S = d.S;
     a.sh = d.cp.stride_h; a.sw = d.cp.stride_w; a.pt = d.cp.pad_top; a.pl = d.cp.pad_left;
     a.dh = d.cp.dil_h; a.dw = d.cp.dil_w;
-    a.K = d.K; a.Kpad = Kpad; a.J = (int)J; a.Jpad = Jpad; a.M = (int)M;
+    a.K = d.K; a.Kpad = Kpad; a.J = (int)Jg; a.Jpad = Jpad; a.M = (int)M;
+    p->C_in = d.C;
+    p->pad_zp = (uint8_t)zpx;
     a.flip4 = d.xt == QNN_UINT8 ? 0x80808080u : 0u;
-    const uint32_t pb = (uint32_t)(uint8_t)(int8_t)zpx_l;
-    a.pad4 = pb | (pb << 8) | (pb << 16) | (pb << 24);
     a.ydt = d.yt;
     a.lo = lo; a.hi = hi;
     a.zp_y = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
     a.rounding = d.rnd;
     a.y_ldc = d.y_ldc; a.y_coff = d.y_coff;
     a.vec_store = (d.y_ldc % 4 == 0) && (d.y_coff % 4 == 0);
-    a.ksteps = ksteps;
-    a.nsplit = nsplit;
     a.tiles_c = tiles_c;
-    a.nblocks = nblocks;
+    a.ntiles = (int)ntiles;
     p->tile = tile;
-    p->avec = gather_width(d.C);
+    p->avec = gather_width(C4);
     p->mode = d.yt == QNN_INT32 ? OUT_INT32 : OUT_REQUANT;
+    a.mode = p->mode;
+    a.fast_rq = fast;
+    a.lo_off = lo + off8;
+    a.hi_off = hi + off8;
+    a.out_xor = off8 ? 0x80808080u : 0u;
+    a.staged = p->mode == OUT_REQUANT && env_int("QNN_STAGED", 1) != 0;
     p->term3 = term3;
-    p->ws_partial_bytes = nsplit > 1 ? align_up((size_t)nsplit * M * Kpad * sizeof(int32_t), 256) : 0;
     p->ws_asum_bytes = term3 ? align_up((size_t)M * sizeof(int32_t), 256) : 0;
-    p->ws_bytes = p->ws_partial_bytes + p->ws_asum_bytes;
-    const TileShape ts = tile_shape(tile);
+    p->ws_xpad_bytes = C4 != d.C ? align_up((size_t)d.N * d.H * d.W * C4, 256) : 0;
+    p->ws_bytes = p->ws_asum_bytes + p->ws_xpad_bytes;
+    // persistent grid: as many workgroups as stay resident, a multiple of 8
+    // (one share per XCD), never more than there are tiles (rounded up)
+    a.chan_in_lds = (size_t)Kpad * sizeof(ChanRec) <= 64 * 1024;
+    const size_t dyn = a.chan_in_lds ? (size_t)Kpad * sizeof(ChanRec) : 0;
+    const int64_t resident = (int64_t)device_cus() * conv_blocks_per_cu(tile, p->avec, dyn);
+    const int64_t grid = std::min<int64_t>((ntiles + 7) / 8 * 8, std::max<int64_t>(8, resident / 8 * 8));
+    a.nblocks = (int)grid;
     char buf[160];
-    snprintf(buf, sizeof buf, "conv_mfma tile=%dx%dx%d gather=%d split=%d blocks=%d term3=%d M=%lld K=%d J=%lld",
-             ts.tc, ts.tp, ts.bk, p->avec, nsplit, nblocks, (int)term3, (long long)M, d.K, (long long)J);
+    snprintf(buf, sizeof buf,
+             "conv_mfma tile=%dx%dx%d gather=%d tiles=%lld grid=%d term3=%d cpad=%d M=%lld K=%d J=%lld",
+             ts.tc, ts.tp, ts.bk, p->avec, (long long)ntiles, a.nblocks, (int)term3, C4 != d.C, (long long)M,
+             d.K, (long long)Jg);
     p->desc = buf;
     *out = p;
     return QNN_OK;
@@ -460,26 +510,32 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
                 ws = p->ws_own;
             if (!ws)
                 return fail(QNN_ERR_NULL, "plan_run: the plan needs a workspace");
-            a.ws = p->ws_partial_bytes ? (int32_t *)ws : nullptr;
-            a.asum = p->term3 ? (const int32_t *)((char *)ws + p->ws_partial_bytes) : nullptr;
+            a.asum = p->term3 ? (const int32_t *)ws : nullptr;
+        }
+        hipError_t e;
+        if (p->ws_xpad_bytes) {
+            uint8_t *xp = (uint8_t *)ws + p->ws_asum_bytes;
+            const long long pixels = (long long)a.N * a.H * a.W;
+            if ((e = launch_pad_channels(a.x, xp, pixels, p->C_in, a.C, p->pad_zp, st)) != hipSuccess)
+                return hip_fail(e, "channel padding launch");
+            a.x = xp;
+            x = xp;
         }
         if (((uintptr_t)x & 15) != 0 && p->avec == 16)
             return fail(QNN_ERR_UNSUPPORTED, "plan_run: x must be 16-byte aligned for C %% 16 == 0");
         if (((uintptr_t)x & 3) != 0 && p->avec == 4)
             return fail(QNN_ERR_UNSUPPORTED, "plan_run: x must be 4-byte aligned for C %% 4 == 0");
+        if (((uintptr_t)x & 7) != 0 && p->avec == 8)
+            return fail(QNN_ERR_UNSUPPORTED, "plan_run: x must be 8-byte aligned for C %% 8 == 0");
         if (a.vec_store && ((uintptr_t)y & (p->mode == OUT_INT32 ? 15 : 3)) != 0)
             a.vec_store = 0;
-        hipError_t e;
+        // whole-row 16-byte stores need a 16-byte aligned row start for every pixel
+        if (a.staged && (((uintptr_t)y & 15) != 0 || a.y_ldc % 16 != 0 || a.y_coff % 16 != 0))
+            a.staged = 0;
         if (p->term3 && (e = launch_window_sums(a, (int32_t *)a.asum, st)) != hipSuccess)
             return hip_fail(e, "window-sum launch");
-        if (a.nsplit > 1) {
-            if ((e = launch_conv(a, p->tile, p->avec, OUT_PARTIAL, st)) != hipSuccess)
-                return hip_fail(e, "conv launch");
-            if ((e = launch_splitk_reduce(a, p->mode, st)) != hipSuccess)
-                return hip_fail(e, "split-K reduce launch");
-        } else if ((e = launch_conv(a, p->tile, p->avec, p->mode, st)) != hipSuccess) {
+        if ((e = launch_conv(a, p->tile, p->avec, st)) != hipSuccess)
             return hip_fail(e, "conv launch");
-        }
         return QNN_OK;
     }
     case PLAN_DW: {

@@ -8,18 +8,21 @@
 namespace qnn {
 
 // Per-output-channel epilogue record of a conv / dense plan.
-//   mult, shift : fixed-point requantize multiplier (shift clamped to <= 63;
-//                 every product with shift >= 63 rounds to 0 anyway)
-//   bconst      : bias[k] - zp_x' * sum_j w[k,j] + J * zp_x' * zp_w[k]
-//                 (terms 2 and 4 of Eq. (3) folded with the bias; int32
-//                 wrap-around arithmetic, exact whenever the true result
-//                 fits int32, which plan creation guarantees)
-//   zpw         : weight zero point (term 3 coefficient)
+//   mult   : fixed-point requantize multiplier (Q31 significand)
+//   bconst : bias[k] - zp_x' * sum_j w[k,j] + J * zp_x' * zp_w[k]
+//            (terms 2 and 4 of Eq. (3) folded with the bias; int32
+//            wrap-around arithmetic, exact whenever the true result fits
+//            int32, which plan creation guarantees)
+//   rndzp  : 32-bit requantize constant 2^(sh-1) + (zp_y + off) * 2^sh with
+//            sh = shift - 32 and off = 128 for int8 outputs (0 for uint8);
+//            only meaningful when the plan uses the 32-bit requantize
+//   shift  : fixed-point shift (clamped to <= 63: every product with a
+//            larger shift rounds to 0 anyway)
 struct ChanRec {
-    int32_t mult, shift, bconst, zpw;
+    int32_t mult, bconst, rndzp, shift;
 };
 
-enum OutMode { OUT_REQUANT = 0, OUT_INT32 = 1, OUT_PARTIAL = 2 };
+enum OutMode { OUT_REQUANT = 0, OUT_INT32 = 1 };
 
 // Implicit-GEMM conv arguments.  GEMM view: D[k][m] = sum_j Wp[k][j] * X'[m][j]
 // with m = output pixel, k = output channel, j = (r*S + s)*C + c.
@@ -27,29 +30,34 @@ struct ConvArgs {
     const uint8_t *x;       // NHWC activations (uint8 or int8 bytes)
     const int8_t *wp;       // packed weights [Kpad][Jpad], zero padded
     const ChanRec *chan;    // [Kpad]
+    const int32_t *zpw;     // [Kpad] weight zero points (term 3)
     const int32_t *asum;    // [M] window sums of x' (term 3) or nullptr
+    const uint8_t *padbuf;  // 16 bytes of zp_x: source of padded / unused gathers
     void *y;                // output (requantized bytes or int32)
-    int32_t *ws;            // split-K partials [nsplit][M][Kpad]
     int32_t N, H, W, C, Ho, Wo, R, S;
     int32_t sh, sw, pt, pl, dh, dw;
     int32_t K, Kpad, J, Jpad, M;
     uint32_t flip4;         // 0x80808080 when x is uint8 (legalised to int8), else 0
-    uint32_t pad4;          // padding byte zp_x' replicated 4 times
     int32_t ydt;            // 0 uint8, 1 int8 (OUT_REQUANT)
     int32_t lo, hi, zp_y, rounding;
     int32_t y_ldc, y_coff;  // in elements
     int32_t vec_store;      // 1 when 4-element groups of y are 4-element aligned
-    int32_t ksteps;         // K-steps (of the tile's BK) per split
-    int32_t nsplit;
     int32_t tiles_c;        // channel tiles
-    int32_t nblocks;        // tiles_c * pixel tiles
+    int32_t ntiles;         // tiles_c * pixel tiles
+    int32_t nblocks;        // persistent grid size (a multiple of 8)
+    int32_t mode;           // OutMode of the conv kernel's epilogue
+    int32_t fast_rq;        // 1: HALF_UP and every shift in [33, 53] (32-bit requantize)
+    int32_t lo_off, hi_off; // output clamp + off (32-bit requantize path)
+    uint32_t out_xor;       // 0x80808080 for int8 outputs of the 32-bit path, else 0
+    int32_t staged;         // 1: 8-bit output staged through LDS, 16-byte row stores
+    int32_t chan_in_lds;    // 1: chan table copied to dynamic LDS (Kpad * 16 bytes)
 };
 
 // Depthwise conv arguments (channel multiplier 1).
 struct DwArgs {
     const uint8_t *x;
     const int32_t *wq;      // [R*S][C] weights minus zero point, int32
-    const ChanRec *chan;    // [C]: mult, shift, bconst (= bias), unused
+    const ChanRec *chan;    // [C]: mult, bconst (= bias), -, shift
     void *y;
     int32_t N, H, W, C, Ho, Wo, R, S;
     int32_t sh, sw, pt, pl, dh, dw;
@@ -82,10 +90,15 @@ struct AddArgs {
 
 // Tile configurations of the MFMA conv kernel.
 enum ConvTile {
-    TILE_128x128 = 0,   // 128 channels x 128 pixels, 2x2 waves of 64x64
-    TILE_64x256 = 1,    // 64 channels x 256 pixels, 1x4 waves of 64x64
-    TILE_256x128 = 2,   // 256 channels x 128 pixels, 2x2 waves of 128x64
-    TILE_64x64 = 3,     // 64 x 64, 2x2 waves of 32x32 (small problems)
+    TILE_128x128 = 0,     // 128 channels x 128 pixels, BK 128, 2x2 waves of 64x64
+    TILE_64x256 = 1,      // 64 channels x 256 pixels, BK 128, 1x4 waves of 64x64
+    TILE_256x128 = 2,     // 256 channels x 128 pixels, BK 128, 2x2 waves of 128x64
+    TILE_64x64 = 3,       // 64 x 64, BK 128, 2x2 waves of 32x32
+    TILE_64x64_K64 = 4,   // 64 x 64, BK 64 (short reductions, J <= 64)
+    TILE_128x128_K64 = 5, // 128 x 128, BK 64
+    TILE_128x64 = 6,      // 128 channels x 64 pixels, BK 128, 2x2 waves of 64x32
+    TILE_64x128 = 7,      // 64 channels x 128 pixels, BK 128, 2x2 waves of 32x64
+    TILE_256x64_K64 = 8,  // 256 channels x 64 pixels, BK 64, 4x1 waves of 64x64
     TILE_COUNT
 };
 
@@ -94,16 +107,20 @@ struct TileShape {
 };
 TileShape tile_shape(int tile);
 
-// Activation gather width in bytes: 16 when C % 16 == 0, else 4 when
-// C % 4 == 0, else 1.
+// Activation gather width in bytes: 16 when C % 16 == 0, 8 when C % 8 == 0,
+// else 4 (C % 4 == 0 after channel padding).
 int gather_width(int C);
 
-hipError_t launch_conv(const ConvArgs &a, int tile, int avec, int mode, hipStream_t st);
-hipError_t launch_splitk_reduce(const ConvArgs &a, int mode, hipStream_t st);
+hipError_t launch_conv(const ConvArgs &a, int tile, int avec, hipStream_t st);
+// Resident workgroups per CU of a conv kernel instantiation (occupancy),
+// given its dynamic LDS bytes.
+int conv_blocks_per_cu(int tile, int avec, size_t dyn_lds);
 hipError_t launch_window_sums(const ConvArgs &a, int32_t *out, hipStream_t st);
-hipError_t launch_prep_conv(const int8_t *w, const int32_t *bias, int K, int J, int Jpad,
-                            int Kpad, int32_t zpx, int8_t *wp, ChanRec *chan, hipStream_t st);
-hipError_t launch_prep_dw(const int8_t *w, const int32_t *bias, int RS, int C, int32_t *wq,
+hipError_t launch_pad_channels(const uint8_t *x, uint8_t *xp, long long pixels, int C, int C4, uint8_t zp,
+                               hipStream_t st);
+hipError_t launch_prep_conv(const int8_t *w, const int32_t *bias, int K, int RS, int C, int C4, int Jpad,
+                            int Kpad, int32_t zpx, int8_t *wp, ChanRec *chan, const int32_t *zpw, hipStream_t st);
+hipError_t launch_prep_dw(const int8_t *w, const int32_t *bias, int RS, int C, const int32_t *zpw, int32_t *wq,
                           ChanRec *chan, hipStream_t st);
 hipError_t launch_depthwise(const DwArgs &a, hipStream_t st);
 hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, hipStream_t st);

@@ -192,18 +192,22 @@ def test_conv_variants(name, layer, N, kw):
     assert_equal(run_gpu(c), run_oracle(c), name)
 
 
-@pytest.mark.parametrize("tile", [0, 1, 2, 3])
-@pytest.mark.parametrize("split", [1, 3])
-def test_every_tile_and_split(tile, split):
-    """Each kernel instantiation (tile shape x split-K), forced, on ragged
-    shapes that span several tiles."""
+@pytest.mark.parametrize("tile", list(range(9)))
+def test_every_tile(tile):
+    """Each kernel instantiation (tile shape x gather width), forced, on
+    ragged shapes that span several tiles, with several tiles per
+    persistent workgroup."""
     layer = W.ConvLayer("t", 23, 21, 64, 200, 3, 3, 1, (1, 1, 1, 1))
-    with env(QNN_TILE=tile, QNN_SPLIT=split):
+    with env(QNN_TILE=tile):
         for kw in ({}, dict(zp_w="channel"), dict(yt="i32")):
-            c = W.conv_case(layer, 2, seed=tile * 10 + split, **kw)
-            assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} split {split} {kw}")
+            c = W.conv_case(layer, 2, seed=tile * 10, **kw)
+            assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} {kw}")
         c = W.conv_case(W.ConvLayer("t", 9, 9, 3, 70, 5, 5, 2, (2, 2, 2, 2)), 3, seed=1)
-        assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} split {split} narrow gather")
+        assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} channel-padded gather")
+        c = W.conv_case(W.ConvLayer("t", 9, 9, 24, 70, 3, 3, 1, (1, 1, 1, 1)), 3, seed=2)
+        assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} 8-byte gather")
+        c = W.conv_case(W.ConvLayer("t", 40, 40, 64, 96, 3, 3, 1, (1, 1, 1, 1)), 8, seed=3)
+        assert_equal(run_gpu(c), run_oracle(c), f"tile {tile} many tiles per workgroup")
 
 
 def test_random_shapes():
@@ -237,13 +241,12 @@ def test_empty_batch_is_noop():
 
 
 def test_plan_workspace_and_streams():
-    """Two runs of one split-K plan on two streams, each with its own
-    workspace, give the oracle's result."""
+    """Two runs of one plan that needs a workspace (window sums of term 3)
+    on two streams, each with its own workspace, give the oracle's result."""
     layer = W.ConvLayer("ws", 7, 7, 512, 512, 3, 3, 1, (1, 1, 1, 1))
     c = W.conv_case(layer, 2, seed=11, zp_w="channel")
     ref = run_oracle(c)
-    with env(QNN_SPLIT=4):
-        p, keep = make_plan(c)
+    p, keep = make_plan(c)
     assert p.workspace_size > 0, p.describe()
     x = dev(c.x)
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
@@ -278,3 +281,22 @@ def test_accumulator_near_int32_bound():
     c.act = None
     c.s_y = 1.0
     assert_equal(run_gpu(c), run_oracle(c), "extreme u8")
+
+
+@pytest.mark.parametrize("staged", [0, 1])
+def test_channel_slice_partial_chunk(staged):
+    """Output written into a channel slice whose width is not a multiple of
+    16 (the staged epilogue's last 16-byte chunk is partial), with both the
+    LDS-staged and the direct store path; channels outside the slice keep
+    their sentinel."""
+    layer = W.ConvLayer("slice", 11, 13, 32, 20, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 3, seed=21)
+    with env(QNN_STAGED=staged):
+        p, keep = make_plan(c, y_ldc=48, y_coff=16)
+    out = torch.full((3, 11, 13, 48), 201, dtype=torch.uint8, device="cuda")
+    p.run(dev(c.x), out=out)
+    torch.cuda.synchronize()
+    p.close()
+    y = out.cpu().numpy()
+    assert (y[..., :16] == 201).all() and (y[..., 36:] == 201).all()
+    assert_equal(y[..., 16:36], run_oracle(c), f"slice staged={staged}")
