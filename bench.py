@@ -227,10 +227,13 @@ def cpu_baseline(workload, target_s=12.0):
             macs += idx.size * c.J
         return macs, time.perf_counter() - t0
 
-    m0, t0 = run(64)
-    per = int(64 * max(1.0, target_s / max(t0, 1e-3)))
-    per = min(per, 200000)
-    macs, t = run(per)
+    # grow the sample until one pass takes about target_s of wall-clock
+    per = 16
+    while True:
+        macs, t = run(per)
+        if t >= 0.6 * target_s or per >= 4000000:
+            break
+        per = min(4000000, int(per * min(16.0, max(2.0, target_s / max(t, 1e-3)))))
     return {"value": round(2.0 * macs / t / 1e12, 6), "unit": "TOP/s", "cores": O.threads(), "kind": "oracle",
             "sample": f"{per} randomly chosen outputs of each of the {len(convs)} layers of the same workload "
                       f"({macs / 1e9:.2f} G MAC in {t:.1f} s, requantize included)"}
@@ -264,7 +267,10 @@ def main():
     ap.add_argument("--workload", default="resnet50_b32")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--layers-out", default=os.path.join(ROOT, "gpurun_out", "bench_layers.json"))
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (3 times), for scaling the "
+                         "FETCH_SIZE / WRITE_SIZE counters, and exit")
+    ap.add_argument("--layers-out", default=None, help="write per-layer timings as JSON to this file")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -273,6 +279,16 @@ def main():
 
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied {n} bytes 3 times")
+        return
     log(f"setting up {args.workload}")
     items, batch = setup(args.workload)
     total_macs = sum(it.macs for it in items)
@@ -316,13 +332,11 @@ def main():
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
         row["gbs"] = round(it.bytes / (float(t) * 1e-3) / 1e9, 1)
         layer_rows.append(row)
-    try:
-        os.makedirs(os.path.dirname(args.layers_out), exist_ok=True)
+    if args.layers_out:
+        os.makedirs(os.path.dirname(os.path.abspath(args.layers_out)), exist_ok=True)
         with open(args.layers_out, "w") as f:
             json.dump({"workload": args.workload, "step_ms": ms, "groups": groups, "layers": layer_rows}, f,
                       indent=1)
-    except OSError:
-        pass
     for r in layer_rows:
         log(f"  {r['layer']:<24} {r['us']:9.2f} us  {r.get('tops', 0):8.1f} TOP/s {r['gbs']:8.1f} GB/s  {r['plan']}")
 

@@ -1,0 +1,169 @@
+"""Condense rocprofv3 CSV output of bench.py into short text summaries.
+
+Reads
+  * a ``--kernel-trace --stats --output-format csv`` directory (kernel_stats.csv),
+  * two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` directories of the same
+    bench command (counter_collection.csv, values in KiB per dispatch),
+  * two more of ``bench.py --calibrate-copy MIB`` (a plain copy of known size),
+  * the per-layer file bench.py writes (algorithmic bytes per kernel group),
+and writes a markdown summary plus ``traffic.json``, which bench.py reads to
+fill ``roofline.traffic`` as long as the conv kernel source is unchanged.
+
+Usage:
+  python -m paper_2006_10226_amd.rocprof_summary --stats D --fetch D --write D \
+      --copy-fetch D --copy-write D --copy-mib 512 --layers F --out-md F \
+      --out-json F --command "..." [--command "..."]
+"""
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import re
+
+_CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
+
+
+def group_of(kernel_name):
+    """bench.py's kernel-group name of a dispatched kernel symbol."""
+    m = _CONV.search(kernel_name)
+    if m:
+        tc, tp, bk, _, _, avec, _ = (int(v) for v in m.groups())
+        return f"conv_mfma tile={tc}x{tp}x{bk} gather={avec}"
+    base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
+    return base
+
+
+def _one(pattern):
+    files = glob.glob(pattern, recursive=True)
+    if not files:
+        raise SystemExit(f"no file matches {pattern}")
+    return files[0]
+
+
+def read_stats(d):
+    rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*kernel_stats.csv")))))
+    out = []
+    for r in rows:
+        out.append({"name": r["Name"], "calls": int(r["Calls"]), "total_ns": float(r["TotalDurationNs"]),
+                    "avg_ns": float(r["AverageNs"]), "pct": float(r["Percentage"]),
+                    "min_ns": float(r["MinNs"]), "max_ns": float(r["MaxNs"])})
+    return out
+
+
+def read_counter(d, counter):
+    """Per kernel group: list of per-dispatch counter values (KiB)."""
+    per = {}
+    vals = {}
+    for r in csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))):
+        if r["Counter_Name"] != counter:
+            continue
+        key = (r["Dispatch_Id"], r["Kernel_Name"])
+        vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+    for (_, name), v in vals.items():
+        per.setdefault(group_of(name), []).append(v)
+    return per
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--stats", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--copy-fetch", required=True)
+    ap.add_argument("--copy-write", required=True)
+    ap.add_argument("--copy-mib", type=int, required=True)
+    ap.add_argument("--layers", required=True)
+    ap.add_argument("--out-md", required=True)
+    ap.add_argument("--out-json", required=True)
+    ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--bench-json", help="the JSON line bench.py printed in the unprofiled run")
+    args = ap.parse_args()
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = open(os.path.join(root, "paper_2006_10226_amd", "csrc", "conv_mfma.hip"), "rb").read()
+    sha = hashlib.sha1(src).hexdigest()
+
+    stats = read_stats(args.stats)
+    layers = json.load(open(args.layers))
+    fetch = read_counter(args.fetch, "FETCH_SIZE")
+    write = read_counter(args.write, "WRITE_SIZE")
+    copy_bytes = args.copy_mib << 20
+    cf = max(read_counter(args.copy_fetch, "FETCH_SIZE").values(), key=len)
+    cw = max(read_counter(args.copy_write, "WRITE_SIZE").values(), key=len)
+    # the copy's largest dispatches are the copy itself
+    f_read = max(cf) * 1024.0 / copy_bytes
+    f_write = max(cw) * 1024.0 / copy_bytes
+
+    groups = {}
+    for g, d in layers["groups"].items():
+        if g not in fetch or g not in write:
+            continue
+        rd = sum(fetch[g]) / len(fetch[g]) * 1024.0 / f_read
+        wr = sum(write[g]) / len(write[g]) * 1024.0 / f_write
+        groups[g] = {"bytes_per_launch": round(rd + wr), "read_bytes_per_launch": round(rd),
+                     "write_bytes_per_launch": round(wr),
+                     "algorithmic_bytes_per_launch": round(d["bytes"] / d["launches"]),
+                     "dispatches_counted": len(fetch[g])}
+    rec = {"source_sha1": sha, "copy_mib": args.copy_mib, "fetch_scale": f_read, "write_scale": f_write,
+           "workload": layers["workload"], "groups": groups}
+    with open(args.out_json, "w") as f:
+        json.dump(rec, f, indent=1)
+
+    by_group = {}
+    for s in stats:
+        g = group_of(s["name"])
+        d = by_group.setdefault(g, {"calls": 0, "total_ns": 0.0, "pct": 0.0})
+        d["calls"] += s["calls"]
+        d["total_ns"] += s["total_ns"]
+        d["pct"] += s["pct"]
+    lines = [f"# rocprofv3 summary: {layers['workload']}", ""]
+    lines.append("Commands (run from the repository root of a copy of this tree):")
+    lines.append("")
+    for c in args.command:
+        lines.append(f"    {c}")
+    lines.append("")
+    lines.append(f"conv_mfma.hip sha1 at the time: `{sha}`")
+    lines.append("")
+    if args.bench_json:
+        lines.append("bench.py line of the unprofiled run:")
+        lines.append("")
+        lines.append("    " + open(args.bench_json).read().strip().splitlines()[-1])
+        lines.append("")
+    lines.append("## Kernel time (--kernel-trace --stats)")
+    lines.append("")
+    lines.append("| kernel group | calls | total ms | avg us | % |")
+    lines.append("|---|---|---|---|---|")
+    for g, d in sorted(by_group.items(), key=lambda kv: -kv[1]["total_ns"]):
+        lines.append(f"| {g} | {d['calls']} | {d['total_ns'] / 1e6:.3f} | {d['total_ns'] / d['calls'] / 1e3:.3f} |"
+                     f" {d['pct']:.1f} |")
+    lines.append("")
+    lines.append("## bench.py per-launch event timing of the same groups (unprofiled run)")
+    lines.append("")
+    lines.append("| kernel group | launches/step | avg us |")
+    lines.append("|---|---|---|")
+    for g, d in layers["groups"].items():
+        lines.append(f"| {g} | {d['launches']} | {d['ms'] / d['launches'] * 1e3:.3f} |")
+    lines.append("")
+    lines.append("## HBM traffic (--pmc FETCH_SIZE, --pmc WRITE_SIZE)")
+    lines.append("")
+    lines.append(f"Copy calibration: a {args.copy_mib} MiB device copy read {max(cf):.0f} KiB and wrote "
+                 f"{max(cw):.0f} KiB per dispatch, so counter KiB x 1024 / {f_read:.4f} (reads) and "
+                 f"/ {f_write:.4f} (writes) give bytes.")
+    lines.append("")
+    lines.append("| kernel group | read MB/launch | write MB/launch | total MB/launch | algorithmic MB/launch |"
+                 " ratio |")
+    lines.append("|---|---|---|---|---|---|")
+    for g, d in groups.items():
+        lines.append(f"| {g} | {d['read_bytes_per_launch'] / 1e6:.3f} | {d['write_bytes_per_launch'] / 1e6:.3f} |"
+                     f" {d['bytes_per_launch'] / 1e6:.3f} | {d['algorithmic_bytes_per_launch'] / 1e6:.3f} |"
+                     f" {d['bytes_per_launch'] / max(1, d['algorithmic_bytes_per_launch']):.2f} |")
+    lines.append("")
+    with open(args.out_md, "w") as f:
+        f.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+if __name__ == "__main__":
+    main()
