@@ -136,8 +136,10 @@ def kernel_group(it):
         return "add"
     if it.kind == "dw":
         return "depthwise"
-    d = dict(kv.split("=") for kv in it.desc.split()[1:] if "=" in kv)
-    return f"conv_mfma tile={d['tile']} gather={d['gather']}"
+    words = it.desc.split()
+    d = dict(kv.split("=") for kv in words[1:] if "=" in kv)
+    extra = f"gather={d['gather']}" if "gather" in d else f"threads={d['threads']} stages={d.get('stages', '')}"
+    return f"{words[0]} tile={d['tile']} {extra}"
 
 
 # ------------------------------------------------------------------ timing

@@ -1,0 +1,207 @@
+// Device helpers shared by the implicit-GEMM conv kernels (conv_tap.hip,
+// conv_dma.hip): LDS swizzle, fixed-point requantize, pixel decode and the
+// tile epilogue.
+#pragma once
+
+#include "qnn_internal.h"
+
+namespace qnn {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+namespace conv {
+
+constexpr int kBufFlags = 0x00020000;   // raw buffer, 32-bit data format
+constexpr int kOutOfRange = (int)0x80000000;
+
+// Physical 16-byte chunk of logical chunk q in an LDS row of CPR chunks; it
+// depends on row & 15 only.  Sixteen lanes reading rows 0..15 at one
+// logical chunk hit 16 distinct 16-byte bank groups (rows of 128 bytes
+// alternate between the two bank halves; rows of 64 bytes cycle through 4).
+template <int CPR>
+__device__ __forceinline__ int swz(int row)
+{
+    if constexpr (CPR == 8)
+        return (row & 7) ^ ((row >> 3) & 1);
+    else
+        return ((row >> 1) & 3) ^ ((row >> 3) & 1);
+}
+
+// n / d for 0 <= n < 2^31 with a host-made magic pair (see make_divider):
+// q = umulhi(n, mul) >> shift, or n itself for d == 1 (mul == 0).
+__device__ __forceinline__ int fast_div(int n, uint32_t mul, uint32_t shift)
+{
+    return mul ? (int)(__umulhi((uint32_t)n, mul) >> shift) : n;
+}
+
+// round(v * mult / 2^shift), 64-bit product; HALF_UP adds 2^(shift-1) and
+// floors, HALF_AWAY adds one less for negative products.
+__device__ __forceinline__ long long round_mul_shift64(int v, int mult, int shift, int away)
+{
+    const long long p = (long long)v * (long long)mult;
+    const long long bias = (1LL << (shift - 1)) - (long long)(away & (int)((unsigned long long)p >> 63));
+    return (p + bias) >> shift;
+}
+
+// Requantize four accumulators of consecutive channels (records rec[e] =
+// {mult, bconst, rndzp, shift}) and pack the output bytes.  The 32-bit form
+// (HALF_UP, 33 <= shift <= 53) is exact: with hi the signed high word of
+// v * mult, floor((v*mult + 2^(shift-1)) / 2^shift) equals
+// floor((hi + 2^(shift-33)) / 2^(shift-32)), and rndzp also carries
+// (zp_y + off) * 2^(shift-32), off = 128 for int8 outputs, which the final
+// XOR removes again.
+__device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v4i (&rec)[4])
+{
+    uint32_t packed = 0;
+    if (a.fast_rq) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int v = (int)((uint32_t)acc[e] + (uint32_t)rec[e].y);
+            const int t = (__mulhi(v, rec[e].x) + rec[e].z) >> (rec[e].w - 32);
+            packed |= (uint32_t)min(max(t, a.lo_off), a.hi_off) << (8 * e);
+        }
+        return packed ^ a.out_xor;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int v = (int)((uint32_t)acc[e] + (uint32_t)rec[e].y);   // wraps exactly when the sum fits
+        long long o = round_mul_shift64(v, rec[e].x, rec[e].w, a.rounding) + a.zp_y;
+        o = o < a.lo ? a.lo : (o > a.hi ? a.hi : o);
+        packed |= ((uint32_t)o & 0xffu) << (8 * e);
+    }
+    return packed;
+}
+
+// Epilogue of one TC x TP tile held by NT/64 waves in a WC x WP grid of
+// (TC/WC) x (TP/WP) wave tiles of 16x16 MFMA blocks: lane holds channels
+// ch..ch+3 (4 * (lane >> 4) inside a 16-block) of pixel lane & 15 inside a
+// 16-block.  Adds the padding correction (when the gather read zeros for
+// taps outside the image) and term 3, then requantizes and stores, through
+// `stage` (LDS, at least TP * (TC + 16) bytes when a.staged) as whole
+// 16-byte pixel-row chunks, or directly.  Every wave must be past its last
+// read of `stage` before the call.
+template <int TC, int TP, int WC, int WP, int STAGE_BYTES>
+__device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC / 16][TP / WP / 16], int8_t *stage,
+                                           int c0, int p0)
+{
+    constexpr int NT = WC * WP * 64;
+    constexpr int WTC = TC / WC, WTP = TP / WP;
+    constexpr int FC = WTC / 16, FP = WTP / 16;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wc = wave / WP, wpos = wave % WP;
+    const int lrow = lane & 15, lchk = lane >> 4;
+    const int mb = p0 + wpos * WTP + lrow;
+
+    if (a.pcorr) {
+        // taps outside the image were gathered as x = 0; the padding value
+        // is zp_x, so add zp_x * (weights of those taps), per border class
+#pragma unroll
+        for (int j = 0; j < FP; ++j) {
+            const int m = mb + j * 16;
+            const int cls = m < a.M ? (int)a.pcls[m] : 255;
+            if (cls != 255) {
+#pragma unroll
+                for (int i = 0; i < FC; ++i) {
+                    const int ch = c0 + wc * WTC + i * 16 + lchk * 4;
+                    acc[i][j] += *(const v4i *)(a.pcorr + (size_t)cls * a.Kpad + ch);
+                }
+            }
+        }
+    }
+    if (a.asum) {
+        // term 3 of Eq. (3): - zp_w[k] * (window sum of x~' at pixel m)
+#pragma unroll
+        for (int i = 0; i < FC; ++i) {
+            const int ch = c0 + wc * WTC + i * 16 + lchk * 4;
+            const v4i zw = *(const v4i *)(a.zpw + ch);
+#pragma unroll
+            for (int j = 0; j < FP; ++j) {
+                const int s3 = a.asum[min(mb + j * 16, a.M - 1)];
+                acc[i][j] -= zw * v4i{s3, s3, s3, s3};
+            }
+        }
+    }
+    if (a.staged) {
+        constexpr int SP = (TP * (TC + 16) <= STAGE_BYTES) ? TC + 16 : TC;
+        static_assert(TP * SP <= STAGE_BYTES, "output staging must fit the LDS buffers");
+#pragma unroll
+        for (int i = 0; i < FC; ++i) {
+            const int cl = wc * WTC + i * 16 + lchk * 4;
+            v4i rec[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                rec[e] = *(const v4i *)(a.chan + c0 + cl + e);
+#pragma unroll
+            for (int j = 0; j < FP; ++j) {
+                const int pl = wpos * WTP + j * 16 + lrow;
+                *(uint32_t *)(stage + pl * SP + cl) = requant4(a, acc[i][j], rec);
+            }
+        }
+        __syncthreads();
+        constexpr int CH = TC / 16;
+        const int kmax = a.K - c0;
+#pragma unroll
+        for (int it = 0; it < (TP * CH + NT - 1) / NT; ++it) {
+            const int idx = it * NT + tid;
+            if (idx < TP * CH) {
+                const int pl = idx / CH, qc = idx % CH;
+                const int m = p0 + pl;
+                if (m < a.M && qc * 16 < kmax) {
+                    const v4i v = *(const v4i *)(stage + pl * SP + qc * 16);
+                    uint8_t *dst = (uint8_t *)a.y + (size_t)m * a.y_ldc + a.y_coff + c0 + qc * 16;
+                    if (qc * 16 + 16 <= kmax) {
+                        *(v4i *)dst = v;
+                    } else {
+                        for (int e = 0; e < kmax - qc * 16; ++e)
+                            dst[e] = (uint8_t)((uint32_t)v[e >> 2] >> (8 * (e & 3)));
+                    }
+                }
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < FC; ++i) {
+        const int ch = c0 + wc * WTC + i * 16 + lchk * 4;
+        if (ch >= a.K)
+            continue;
+        const bool full = a.vec_store && ch + 3 < a.K;
+        v4i rec[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            rec[e] = *(const v4i *)(a.chan + ch + e);
+#pragma unroll
+        for (int j = 0; j < FP; ++j) {
+            const int m = mb + j * 16;
+            if (m >= a.M)
+                continue;
+            const size_t off = (size_t)m * a.y_ldc + a.y_coff + ch;
+            if (a.mode == OUT_INT32) {
+                int vals[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    vals[e] = (int)((uint32_t)acc[i][j][e] + (uint32_t)rec[e].y);
+                int32_t *yp = (int32_t *)a.y + off;
+                if (full) {
+                    *(v4i *)yp = v4i{vals[0], vals[1], vals[2], vals[3]};
+                } else {
+                    for (int e = 0; e < 4 && ch + e < a.K; ++e)
+                        yp[e] = vals[e];
+                }
+                continue;
+            }
+            const uint32_t packed = requant4(a, acc[i][j], rec);
+            uint8_t *yp = (uint8_t *)a.y + off;
+            if (full) {
+                *(uint32_t *)yp = packed;
+            } else {
+                for (int e = 0; e < 4 && ch + e < a.K; ++e)
+                    yp[e] = (uint8_t)(packed >> (8 * e));
+            }
+        }
+    }
+}
+
+}  // namespace conv
+}  // namespace qnn

@@ -1,0 +1,348 @@
+// Implicit-GEMM quantized conv2d / dense with operands streamed straight
+// into LDS (gfx950 buffer loads with the LDS-direct bit), for channel
+// counts that are a multiple of 64.
+//
+// Arithmetic as in conv_mfma.hip (Jain et al., Sec. II-B Eq. (3), Sec.
+// III-B/C): term 1 on int8 MFMA over x' = x - 128 (uint8 inputs) or x
+// (int8), terms 2 and 4 and the bias folded into ChanRec.bconst, term 3
+// from the window sums, requantize of Eq. (5) in the epilogue.
+//
+// What differs is the data path.  Every K-step is a 64-byte channel slice
+// of one filter tap (C % 64 == 0), so each 16-byte chunk of the gather has
+// the address  x + pixel_base(m) + tap_offset(r, s) + cc + 16 * q  and is
+// fetched by one lane of a buffer load whose destination is LDS: a wave
+// writes 1 KB (16 rows x 64 bytes) per instruction, lane L landing at byte
+// 16 * L, so each lane fetches the chunk that the XOR swizzle places there.
+// No registers hold staged tiles, so NS stages (NS - 1 of them in flight)
+// cover the memory latency, with one barrier per K-step.
+//
+// Two consequences of skipping the registers:
+//   * the uint8 -> int8 flip (XOR 0x80 per byte) is applied to the
+//     activation fragments after they are read from LDS;
+//   * a tap outside the image is fetched from an out-of-range offset, which
+//     the hardware answers with zero bytes, i.e. x = 0 instead of the
+//     padding value zp_x.  The difference, zp_x times the sum of the
+//     weights of the outside taps, depends only on which taps are outside
+//     (the pixel's border class) and the channel; the plan tabulates it
+//     and the epilogue adds it (store_tile).
+#include "conv_common.h"
+
+namespace qnn {
+
+using namespace conv;
+
+namespace {
+
+// s_waitcnt with only the vector-memory count set (gfx9 encoding: vmcnt
+// low bits 3:0 and high bits 15:14, expcnt 6:4 and lgkmcnt 11:8 at their
+// no-wait maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier for the stage ring: this wave's LDS-direct loads up to
+// the stage about to be read have landed (vmcnt N) and its LDS reads of the
+// stage about to be overwritten have returned (lgkmcnt 0) before it
+// arrives.  A plain __syncthreads would also wait for the loads still in
+// flight (they write LDS), draining the pipeline at every K-step.
+template <int N>
+__device__ __forceinline__ void stage_barrier()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Swizzle of 64-byte LDS rows: physical chunk = logical chunk ^ sw64(row).
+// Measured on gfx950 (bank-conflict counter): with it, the 64 lanes of an
+// operand read (row L % 16, chunk L / 16) are conflict free.
+__device__ __forceinline__ int sw64(int row)
+{
+    return (row >> 1) & 3;
+}
+
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, int8_t *lds_dst, int voff, int soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds_dst, 16, voff, soff, 0,
+                                             0);
+}
+
+}  // namespace
+
+template <int WTC, int WTP>
+constexpr int dma_occupancy()
+{
+    return WTC * WTP >= 128 * 64 ? 1 : 2;
+}
+
+template <int TC, int TP, int WC, int WP, int NS, bool FLIP>
+__global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>())) conv_dma_kernel(ConvArgs a)
+{
+    constexpr int NW = WC * WP;
+    constexpr int BK = 64;
+    constexpr int WTC = TC / WC, WTP = TP / WP;
+    constexpr int FC = WTC / 16, FP = WTP / 16;
+    constexpr int STAGE = (TC + TP) * BK;
+    constexpr int LA = TC / (16 * NW);   // 1 KB weight blocks per wave per stage
+    constexpr int LB = TP / (16 * NW);   // 1 KB activation blocks per wave per stage
+    constexpr int LPS = LA + LB;         // loads per lane per stage
+    constexpr int LDS_BYTES = NS * STAGE > TP * (TC + 16) ? NS * STAGE : TP * (TC + 16);
+    static_assert(TC % (16 * NW) == 0 && TP % (16 * NW) == 0, "every wave loads whole 16-row blocks");
+    static_assert((NS & (NS - 1)) == 0 && NS >= 2, "stage count is a power of two");
+    static_assert(LPS * (NS - 2) < 64, "vmcnt range");
+    static_assert(NS >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
+
+    __shared__ __attribute__((aligned(1024))) int8_t lds[LDS_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wc = wave / WP, wpos = wave % WP;
+
+    // XCD x (workgroups dealt round-robin) takes the x-th eighth of the
+    // tile list; consecutive tiles are the channel tiles of one pixel tile.
+    const int chunk = (a.ntiles + 7) >> 3;
+    const int xcd = blockIdx.x & 7;
+    const int tile = xcd * chunk + (blockIdx.x >> 3);
+    if (tile >= min(a.ntiles, (xcd + 1) * chunk))
+        return;
+    const int c0 = (tile % a.tiles_c) * TC;
+    const int p0 = (tile / a.tiles_c) * TP;
+
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0, a.N * a.H * a.W * a.C, kBufFlags);
+    const __amdgpu_buffer_rsrc_t rw =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, (short)0, a.Kpad * a.Jpad, kBufFlags);
+
+    // A 16-row x 64-byte block: lane L of the LDS-direct load that writes
+    // it lands at byte 16 * L, i.e. row L / 4, physical chunk L % 4, and
+    // fetches logical chunk (L % 4) ^ sw(row), so four consecutive lanes
+    // read one 64-byte run of global memory.  The operand reads (lane L:
+    // row L % 16, logical chunk L / 16) are then free of bank conflicts.
+    const int r16 = lane >> 2, pch = lane & 3;
+    int voffA[LA];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+        const int row = (i * NW + wave) * 16 + r16;
+        voffA[i] = (c0 + row) * a.Jpad + ((pch ^ sw64(row)) << 4);
+    }
+    int pbase[LB];
+    uint32_t pmask[LB];
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int row = (i * NW + wave) * 16 + r16;
+        const int m = p0 + row;
+        pbase[i] = 0;
+        pmask[i] = 0;
+        if (m < a.M) {
+            const int t = fast_div(m, a.mWo, a.sWo);
+            const int ow = m - t * a.Wo;
+            const int n = fast_div(t, a.mHo, a.sHo);
+            const int oh = t - n * a.Ho;
+            const int ih0 = oh * a.sh - a.pt, iw0 = ow * a.sw - a.pl;
+            pbase[i] = ((n * a.H + ih0) * a.W + iw0) * a.C + ((pch ^ sw64(row)) << 4);
+            uint32_t rm = 0, cm = 0;
+            for (int r = 0; r < a.R; ++r)
+                rm |= (uint32_t)((unsigned)(ih0 + r * a.dh) < (unsigned)a.H) << r;
+            for (int s = 0; s < a.S; ++s)
+                cm |= (uint32_t)((unsigned)(iw0 + s * a.dw) < (unsigned)a.W) << s;
+            pmask[i] = rm | (cm << 16);
+        }
+    }
+
+    // ---- loader: tap (lr, ls) and channel offset lc of the next stage ---
+    const int nk = a.nk;
+    int lr = 0, ls = 0, lc = 0;
+    int voffB[LB];
+    auto set_tap = [&]() {
+        const int toff = (lr * a.dh * a.W + ls * a.dw) * a.C;
+        const uint32_t rin = lr < a.R ? 1u : 0u;
+#pragma unroll
+        for (int i = 0; i < LB; ++i) {
+            const bool v = (pmask[i] >> lr) & (pmask[i] >> (16 + ls)) & rin;
+            voffB[i] = v ? pbase[i] + toff : kOutOfRange;
+        }
+    };
+    // Stages past the end are issued too (out of range: zeros, no memory
+    // traffic), so every K-step waits for the same count.  Out of range is
+    // signalled in the VGPR offset (>= 2^31) with a small scalar offset.
+    auto issue = [&](int ks) {
+        int8_t *base = lds + (ks & (NS - 1)) * STAGE;
+        const bool live = ks < nk;
+        const int soffA = __builtin_amdgcn_readfirstlane(live ? ks * BK : 0);
+        const int oobA = __builtin_amdgcn_readfirstlane(live ? 0 : kOutOfRange);
+        const int soffB = __builtin_amdgcn_readfirstlane(lc);
+#pragma unroll
+        for (int i = 0; i < LA; ++i)
+            dma16(rw, base + (i * NW + wave) * 16 * BK, voffA[i] | oobA, soffA);
+#pragma unroll
+        for (int i = 0; i < LB; ++i)
+            dma16(rx, base + TC * BK + (i * NW + wave) * 16 * BK, voffB[i], soffB);
+        lc += BK;
+        if (lc == a.C) {
+            lc = 0;
+            if (++ls == a.S) {
+                ls = 0;
+                ++lr;   // lr == R past the last tap: every row reads out of range
+            }
+            set_tap();
+        }
+    };
+
+    // ---- fragments and MFMAs ------------------------------------------
+    const int lrow = lane & 15, lchk = lane >> 4;
+    const int co = (lchk ^ sw64(lrow)) << 4;
+    v4i acc[FC][FP];
+#pragma unroll
+    for (int i = 0; i < FC; ++i)
+#pragma unroll
+        for (int j = 0; j < FP; ++j)
+            acc[i][j] = v4i{0, 0, 0, 0};
+    v4i fa[2][FC], fb[2][FP];
+    auto read_frags = [&](int ks, v4i (&A)[FC], v4i (&B)[FP]) {
+        const int8_t *As = lds + (ks & (NS - 1)) * STAGE + (wc * WTC + lrow) * BK + co;
+        const int8_t *Bs = lds + (ks & (NS - 1)) * STAGE + TC * BK + (wpos * WTP + lrow) * BK + co;
+#pragma unroll
+        for (int i = 0; i < FC; ++i)
+            A[i] = *(const v4i *)(As + i * 16 * BK);
+#pragma unroll
+        for (int j = 0; j < FP; ++j)
+            B[j] = *(const v4i *)(Bs + j * 16 * BK);
+    };
+    auto mfma = [&](const v4i (&A)[FC], v4i (&B)[FP]) {
+        if constexpr (FLIP) {
+#pragma unroll
+            for (int j = 0; j < FP; ++j)
+                B[j] ^= v4i{(int)0x80808080, (int)0x80808080, (int)0x80808080, (int)0x80808080};
+        }
+#pragma unroll
+        for (int i = 0; i < FC; ++i)
+#pragma unroll
+            for (int j = 0; j < FP; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[i], B[j], acc[i][j], 0, 0, 0);
+    };
+
+    // ---- pipeline ---------------------------------------------------------
+    // NS - 1 stages of loads in flight; the fragments of stage k + 1 are
+    // read from LDS while the MFMAs of stage k run.  The barrier of step k
+    // certifies that stage k + 1 has landed everywhere and that every wave
+    // is done with step k - 1, so buffer (k - 1) mod NS takes stage
+    // k + NS - 1.
+    set_tap();
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        issue(s);
+    stage_barrier<LPS *(NS - 2)>();
+    read_frags(0, fa[0], fb[0]);
+    int k = 0;
+    for (; k + 2 <= nk; k += 2) {
+        stage_barrier<LPS *(NS - 3)>();
+        issue(k + NS - 1);
+        read_frags(k + 1, fa[1], fb[1]);
+        mfma(fa[0], fb[0]);
+        stage_barrier<LPS *(NS - 3)>();
+        issue(k + NS);
+        read_frags(k + 2, fa[0], fb[0]);
+        mfma(fa[1], fb[1]);
+    }
+    if (k < nk)
+        mfma(fa[0], fb[0]);
+    wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
+    __syncthreads();
+    store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0);
+}
+
+// Padding correction table of the border classes (plan preparation): one
+// thread per (class, channel) sums the packed weights of the taps outside
+// the image and scales by zp_x.  The result wraps to int32 like every other
+// term of the accumulator, which is exact whenever the final sum fits.
+__global__ void __launch_bounds__(256) border_corr_kernel(const int8_t *wp, int Kpad, int Jpad, int C4, int S, int RS,
+                                                          const uint32_t *rmask, const uint32_t *cmask, int ncls,
+                                                          int32_t zpx, int32_t *corr)
+{
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= ncls * Kpad)
+        return;
+    const int cls = idx / Kpad, k = idx - cls * Kpad;
+    long long sum = 0;
+    for (int t = 0; t < RS; ++t) {
+        const int r = t / S, s = t - r * S;
+        if (((rmask[cls] >> r) & (cmask[cls] >> s) & 1u) == 0) {
+            const int8_t *row = wp + (size_t)k * Jpad + (size_t)t * C4;
+            for (int c = 0; c < C4; ++c)
+                sum += row[c];
+        }
+    }
+    corr[idx] = (int32_t)(uint32_t)(unsigned long long)(sum * zpx);
+}
+
+hipError_t launch_border_corr(const int8_t *wp, int Kpad, int Jpad, int C4, int S, int RS, const uint32_t *rmask,
+                              const uint32_t *cmask, int ncls, int32_t zpx, int32_t *corr, hipStream_t st)
+{
+    const int n = ncls * Kpad;
+    hipLaunchKernelGGL(border_corr_kernel, dim3((n + 255) / 256), dim3(256), 0, st, wp, Kpad, Jpad, C4, S, RS, rmask,
+                       cmask, ncls, zpx, corr);
+    return hipGetLastError();
+}
+
+// DmaTile -> tile, wave grid and stage count.
+struct DmaCfg {
+    int tc, tp, wc, wp, ns;
+};
+static constexpr DmaCfg kDmaCfg[DMA_COUNT] = {
+    {128, 128, 2, 2, 4}, {128, 128, 2, 2, 8}, {128, 64, 2, 2, 4}, {64, 128, 2, 2, 4},
+    {64, 64, 2, 2, 4},   {256, 128, 4, 2, 4}, {128, 256, 2, 4, 4}, {128, 64, 2, 2, 8},
+    {256, 128, 2, 2, 4}, {128, 256, 2, 2, 4}, {128, 128, 1, 2, 8}, {128, 128, 2, 1, 8},
+    {64, 64, 2, 2, 8},   {64, 128, 2, 2, 8},  {64, 64, 2, 2, 16},
+};
+
+TileShape dma_tile_shape(int tile)
+{
+    return {kDmaCfg[tile].tc, kDmaCfg[tile].tp, 64};
+}
+
+int dma_threads(int tile)
+{
+    return kDmaCfg[tile].wc * kDmaCfg[tile].wp * 64;
+}
+
+int dma_stages(int tile)
+{
+    return kDmaCfg[tile].ns;
+}
+
+template <int T>
+static hipError_t launch_dma_cfg(const ConvArgs &a, hipStream_t st)
+{
+    constexpr DmaCfg c = kDmaCfg[T];
+    const int grid = (a.ntiles + 7) / 8 * 8;
+    if (a.flip4)
+        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true>), dim3(grid),
+                           dim3(c.wc * c.wp * 64), 0, st, a);
+    else
+        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false>), dim3(grid),
+                           dim3(c.wc * c.wp * 64), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int T>
+static hipError_t launch_dma_from(const ConvArgs &a, int tile, hipStream_t st)
+{
+    if constexpr (T < DMA_COUNT) {
+        if (tile == T)
+            return launch_dma_cfg<T>(a, st);
+        return launch_dma_from<T + 1>(a, tile, st);
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st)
+{
+    return launch_dma_from<0>(a, tile, st);
+}
+
+}  // namespace qnn

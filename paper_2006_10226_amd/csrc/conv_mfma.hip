@@ -182,7 +182,7 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
     const int t_first = xcd * chunk + lb;
     const int t_end = min(a.ntiles, (xcd + 1) * chunk);
     const int my_tiles = t_first < t_end ? (t_end - t_first + gx - 1) / gx : 0;
-    const int nk = a.Jpad / BK;
+    const int nk = a.nk;
     const int G = my_tiles * nk;
     if (G == 0)
         return;

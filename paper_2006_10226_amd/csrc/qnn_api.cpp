@@ -136,11 +136,19 @@ enum PlanKind { PLAN_CONV = 0, PLAN_DW = 1, PLAN_REQ = 2 };
 
 }  // namespace
 
+// One implicit-GEMM kernel configuration: family and tile enum value.
+enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2 };
+struct ConvKernel {
+    int fam = FAM_GATHER;
+    int tile = TILE_64x64;
+};
+
 struct qnn_plan {
     PlanKind kind;
     // conv / dense
     ConvArgs conv{};
-    int tile = 0, avec = 16, mode = OUT_REQUANT;
+    int avec = 16, mode = OUT_REQUANT;
+    ConvKernel ker;             // kernel family and tile that run_plan launches
     bool term3 = false;
     size_t ws_asum_bytes = 0, ws_xpad_bytes = 0;
     int32_t C_in = 0;           // channels of the caller's x (before padding to a.C)
@@ -281,16 +289,228 @@ qnn_status read_bias(const int32_t *bias, int n, hipStream_t st, std::vector<int
     return QNN_OK;
 }
 
-// Tile choice for an implicit-GEMM problem of M pixels x K channels x J
-// reduction (QNN_TILE overrides it for sweeps).
-int choose_tile(int64_t M, int K, int J)
+TileShape kernel_shape(const ConvKernel &k)
 {
-    const int t = env_int("QNN_TILE", -1);
-    if (t >= 0 && t < TILE_COUNT)
-        return t;
+    switch (k.fam) {
+    case FAM_DMA: return dma_tile_shape(k.tile);
+    case FAM_TAP: return tap_tile_shape(k.tile);
+    default: return tile_shape(k.tile);
+    }
+}
+
+// Candidate kernels for a conv of M pixels x K channels with C4 channels
+// per tap and reduction J.  QNN_DMA / QNN_TAP / QNN_TILE=<n> force one
+// configuration when it is eligible (for sweeps and tests).
+std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool tap_ok, bool dma_ok)
+{
     (void)M;
     (void)K;
-    return J <= 64 ? TILE_64x64_K64 : TILE_64x64;
+    std::vector<ConvKernel> c;
+    const int f_dma = env_int("QNN_DMA", -1), f_tap = env_int("QNN_TAP", -1), f_tile = env_int("QNN_TILE", -1);
+    if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok)
+        return {{FAM_DMA, f_dma}};
+    if (f_tap >= 0 && f_tap < TAP_COUNT && tap_ok && C4 % tap_tile_shape(f_tap).bk == 0)
+        return {{FAM_TAP, f_tap}};
+    if (f_tile >= 0 && f_tile < TILE_COUNT)
+        return {{FAM_GATHER, f_tile}};
+    if (dma_ok && env_int("QNN_DMA", -1) != -2)
+        for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_256x128_S4, DMA_128x256_S4,
+                      DMA_128x128_S8, DMA_128x64_S8, DMA_64x64_S8, DMA_64x128_S8, DMA_64x64_S16})
+            c.push_back({FAM_DMA, t});
+    if (c.empty()) {
+        // the general gather kernel: short reductions use the 64-deep K-step
+        c.push_back({FAM_GATHER, J <= 64 ? TILE_64x64_K64 : TILE_64x64});
+        for (int t : {TILE_64x64_K64, TILE_64x128, TILE_128x64, TILE_128x128})
+            if (t != c[0].tile)
+                c.push_back({FAM_GATHER, t});
+    }
+    return c;
+}
+
+int device_cus();
+
+// Tiling of the launched kernel: tile counts, K-steps, persistent grid.
+// The padding correction tables (pcorr_tab, pcls_tab) belong to the
+// LDS-direct kernel only: the other families gather zp_x themselves.
+void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr_tab, const uint8_t *pcls_tab)
+{
+    const TileShape ts = kernel_shape(k);
+    a.pcorr = k.fam == FAM_DMA ? pcorr_tab : nullptr;
+    a.pcls = k.fam == FAM_DMA ? pcls_tab : nullptr;
+    const int64_t tiles_c = (a.K + ts.tc - 1) / ts.tc;
+    const int64_t ntiles = tiles_c * (((int64_t)a.M + ts.tp - 1) / ts.tp);
+    a.tiles_c = (int)tiles_c;
+    a.ntiles = ntiles < (int64_t(1) << 31) - 8 ? (int)ntiles : -1;
+    a.nk = (a.J + ts.bk - 1) / ts.bk;
+    a.nblocks = 0;
+    if (k.fam == FAM_GATHER && a.ntiles >= 0) {
+        // persistent grid: as many workgroups as stay resident, a multiple
+        // of 8 (one share per XCD), never more than there are tiles
+        const size_t dyn = a.chan_in_lds ? (size_t)a.Kpad * sizeof(ChanRec) : 0;
+        const int64_t resident = (int64_t)device_cus() * conv_blocks_per_cu(k.tile, avec, dyn);
+        a.nblocks = (int)std::min<int64_t>((ntiles + 7) / 8 * 8, std::max<int64_t>(8, resident / 8 * 8));
+    }
+}
+
+hipError_t launch_conv_kernel(const ConvArgs &a, const ConvKernel &k, int avec, hipStream_t st)
+{
+    switch (k.fam) {
+    case FAM_DMA: return launch_conv_dma(a, k.tile, st);
+    case FAM_TAP: return launch_conv_tap(a, k.tile, st);
+    default: return launch_conv(a, k.tile, avec, st);
+    }
+}
+
+// Times every candidate on the plan's shape and returns the fastest.
+// Scratch activations (a constant fill), output and window sums are
+// allocated for the measurement and freed again.
+qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &cands, int avec, bool term3,
+                         const int32_t *pcorr_tab, const uint8_t *pcls_tab, hipStream_t st, ConvKernel *best)
+{
+    const size_t xb = align_up((size_t)base.N * base.H * base.W * base.C, 256);
+    const size_t elem = base.mode == OUT_INT32 ? 4 : 1;
+    const size_t yb = align_up((size_t)base.M * base.y_ldc * elem, 256);
+    const size_t sb = align_up((size_t)base.M * sizeof(int32_t), 256);
+    void *buf = nullptr;
+    hipError_t e = hipMalloc(&buf, xb + yb + sb);
+    if (e != hipSuccess)
+        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes for kernel tuning failed", xb + yb + sb);
+    // Each timed launch starts with cold caches, as a layer does inside a
+    // network: a fill larger than the L2s and the 256 MB last-level cache
+    // runs before it.  (Without the buffer the timing is warm.)
+    const size_t flush_bytes = size_t(320) << 20;
+    void *flush = nullptr;
+    if (hipMalloc(&flush, flush_bytes) != hipSuccess)
+        flush = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    qnn_status s = QNN_OK;
+    float best_ms = 1e30f;
+    ConvArgs a = base;
+    a.x = (const uint8_t *)buf;
+    a.y = (char *)buf + xb;
+    a.asum = term3 ? (const int32_t *)((char *)buf + xb + yb) : nullptr;
+    if ((e = hipMemsetAsync(buf, 0x35, xb + yb + sb, st)) != hipSuccess || (e = hipEventCreate(&e0)) != hipSuccess ||
+        (e = hipEventCreate(&e1)) != hipSuccess) {
+        s = hip_fail(e, "kernel tuning set-up");
+    } else {
+        for (const ConvKernel &k : cands) {
+            set_tiling(a, k, avec, pcorr_tab, pcls_tab);
+            if (a.ntiles < 0)
+                continue;
+            float t = 0;
+            // one untimed launch, then the median of three cold launches
+            if ((e = launch_conv_kernel(a, k, avec, st)) != hipSuccess)
+                break;
+            float runs[3];
+            for (int r = 0; r < 3 && e == hipSuccess; ++r) {
+                if (flush && (e = hipMemsetAsync(flush, r, flush_bytes, st)) != hipSuccess)
+                    break;
+                if ((e = hipEventRecord(e0, st)) != hipSuccess || (e = launch_conv_kernel(a, k, avec, st)) != hipSuccess ||
+                    (e = hipEventRecord(e1, st)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess ||
+                    (e = hipEventElapsedTime(&runs[r], e0, e1)) != hipSuccess)
+                    break;
+            }
+            if (e != hipSuccess)
+                break;
+            std::sort(runs, runs + 3);
+            t = runs[1];
+            if (t < best_ms) {
+                best_ms = t;
+                *best = k;
+            }
+        }
+        if (e != hipSuccess)
+            s = hip_fail(e, "kernel tuning");
+    }
+    if (e0)
+        (void)hipEventDestroy(e0);
+    if (e1)
+        (void)hipEventDestroy(e1);
+    (void)hipStreamSynchronize(st);
+    (void)hipFree(buf);
+    if (flush)
+        (void)hipFree(flush);
+    return s;
+}
+
+// Magic pair for n / d with 0 <= n < 2^31: with l = ceil(log2 d) and
+// mul = ceil(2^(31+l) / d) < 2^32, n * mul / 2^(31+l) exceeds n / d by less
+// than 2^-l <= 1/d, which never reaches the next integer, so
+// n / d = umulhi(n, mul) >> (l - 1).  d == 1 is flagged by mul == 0.
+void make_divider(uint32_t d, uint32_t &mul, uint32_t &shift)
+{
+    if (d <= 1) {
+        mul = 0;
+        shift = 0;
+        return;
+    }
+    int l = 0;
+    while ((1ull << l) < d)
+        ++l;
+    mul = (uint32_t)(((1ull << (31 + l)) + d - 1) / d);
+    shift = (uint32_t)(l - 1);
+}
+
+// Border classes of the output pixels: the set of filter taps that fall
+// outside the image depends on the output row through a row mask (valid
+// r) and on the column through a column mask (valid s).  Each distinct
+// (row mask, column mask) pair with an outside tap is a class; pixels with
+// every tap inside get 255.
+struct BorderClasses {
+    std::vector<uint8_t> pcls;           // [M]
+    std::vector<uint32_t> rmask, cmask;  // per class
+    bool any = false;
+};
+
+bool border_classes(const ConvDesc &d, int Ho, int Wo, int64_t M, BorderClasses &bc)
+{
+    const uint32_t full_r = (1u << d.R) - 1, full_c = (1u << d.S) - 1;
+    std::vector<uint32_t> ru, cu;
+    std::vector<int> rcls(Ho), ccls(Wo);
+    for (int oh = 0; oh < Ho; ++oh) {
+        uint32_t m = 0;
+        for (int r = 0; r < d.R; ++r) {
+            const int64_t ih = (int64_t)oh * d.cp.stride_h - d.cp.pad_top + (int64_t)r * d.cp.dil_h;
+            m |= (uint32_t)(ih >= 0 && ih < d.H) << r;
+        }
+        const auto it = std::find(ru.begin(), ru.end(), m);
+        rcls[oh] = (int)(it - ru.begin());
+        if (it == ru.end())
+            ru.push_back(m);
+    }
+    for (int ow = 0; ow < Wo; ++ow) {
+        uint32_t m = 0;
+        for (int s = 0; s < d.S; ++s) {
+            const int64_t iw = (int64_t)ow * d.cp.stride_w - d.cp.pad_left + (int64_t)s * d.cp.dil_w;
+            m |= (uint32_t)(iw >= 0 && iw < d.W) << s;
+        }
+        const auto it = std::find(cu.begin(), cu.end(), m);
+        ccls[ow] = (int)(it - cu.begin());
+        if (it == cu.end())
+            cu.push_back(m);
+    }
+    const size_t ncls = ru.size() * cu.size();
+    if (ncls > 255)
+        return false;
+    bc.rmask.resize(ncls);
+    bc.cmask.resize(ncls);
+    std::vector<uint8_t> id(ncls);
+    for (size_t rc = 0; rc < ru.size(); ++rc)
+        for (size_t cc = 0; cc < cu.size(); ++cc) {
+            const size_t c = rc * cu.size() + cc;
+            bc.rmask[c] = ru[rc];
+            bc.cmask[c] = cu[cc];
+            const bool interior = ru[rc] == full_r && cu[cc] == full_c;
+            id[c] = interior ? 255 : (uint8_t)c;
+            bc.any |= !interior;
+        }
+    bc.pcls.resize((size_t)M);
+    size_t m = 0;
+    for (int n = 0; n < d.N; ++n)
+        for (int oh = 0; oh < Ho; ++oh)
+            for (int ow = 0; ow < Wo; ++ow)
+                bc.pcls[m++] = id[(size_t)rcls[oh] * cu.size() + ccls[ow]];
+    return true;
 }
 
 int device_cus()
@@ -379,14 +599,22 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     const int C4 = (d.C + 3) / 4 * 4;
     const int RS = d.R * d.S;
     const int64_t Jg = (int64_t)RS * C4;   // GEMM reduction length
-    const int tile = choose_tile(M, d.K, (int)Jg);
-    const TileShape ts = tile_shape(tile);
-    const int Kpad = (int)align_up(d.K, ts.tc);
-    const int Jpad = (int)align_up(Jg, ts.bk);
-    const int tiles_c = Kpad / ts.tc;
-    const int64_t ntiles = tiles_c * ((M + ts.tp - 1) / ts.tp);
-    if (ntiles >= (int64_t(1) << 31))
-        return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
+    // weights are packed once for every kernel: rows padded to the largest
+    // channel tile, the row stride to the largest K-step
+    const int Kpad = (int)align_up(d.K, 256);
+    const int Jpad = (int)align_up(Jg, 128);
+    if ((int64_t)Kpad * Jpad >= (int64_t(1) << 31)) {
+        free_plan(p);
+        return fail(QNN_ERR_UNSUPPORTED, "packed weights of 2^31 bytes or more are not supported");
+    }
+    // the tap kernels gather one filter tap per K-step (C4 % BK == 0); the
+    // LDS-direct one also needs the border classes for its padding fix-up
+    BorderClasses bc;
+    const bool tap_ok = C4 % 64 == 0 && d.R <= 16 && d.S <= 16;
+    const bool dma_ok = tap_ok && border_classes(d, Ho, Wo, M, bc);
+    const bool pcorr = dma_ok && bc.any && zpx != 0;
+    const size_t ncls = pcorr ? bc.rmask.size() : 0;
+    const std::vector<ConvKernel> cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok);
     const bool term3 = [&] {
         for (int i = 0; i < d.wq.n; ++i)
             if (d.wq.zero_point[i] != 0)
@@ -407,7 +635,10 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     const size_t ch_bytes = align_up(sizeof(ChanRec) * Kpad, 256);
     const size_t zw_bytes = align_up(sizeof(int32_t) * Kpad, 256);
     const size_t pad_bytes = 256;
-    const size_t total = wp_bytes + ch_bytes + zw_bytes + pad_bytes;
+    const size_t pcls_bytes = pcorr ? align_up((size_t)M, 256) : 0;
+    const size_t corr_bytes = pcorr ? align_up(sizeof(int32_t) * ncls * Kpad, 256) : 0;
+    const size_t mask_bytes = pcorr ? align_up(sizeof(uint32_t) * 2 * ncls, 256) : 0;
+    const size_t total = wp_bytes + ch_bytes + zw_bytes + pad_bytes + pcls_bytes + corr_bytes + mask_bytes;
     hipError_t e = hipMalloc(&p->dev, total);
     if (e != hipSuccess) {
         free_plan(p);
@@ -436,9 +667,22 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         std::memcpy(host.data() + ch_bytes + sizeof(int32_t) * k, &z, sizeof z);
     }
     std::memset(host.data() + ch_bytes + zw_bytes, (uint8_t)zpx, pad_bytes);
+    uint8_t *pcls_d = padbuf + pad_bytes;
+    int32_t *corr_d = (int32_t *)(pcls_d + pcls_bytes);
+    uint32_t *mask_d = (uint32_t *)((char *)corr_d + corr_bytes);
+    std::vector<uint32_t> masks;
+    if (pcorr) {
+        masks = bc.rmask;
+        masks.insert(masks.end(), bc.cmask.begin(), bc.cmask.end());
+    }
     if ((e = hipMemcpyAsync(chan, host.data(), host.size(), hipMemcpyHostToDevice, st)) != hipSuccess ||
         (e = launch_prep_conv(d.w, d.bias, d.K, RS, d.C, C4, Jpad, Kpad, zpx_l, wp, chan, zpw_d, st)) !=
             hipSuccess ||
+        (pcorr && ((e = hipMemcpyAsync(pcls_d, bc.pcls.data(), (size_t)M, hipMemcpyHostToDevice, st)) != hipSuccess ||
+                   (e = hipMemcpyAsync(mask_d, masks.data(), sizeof(uint32_t) * masks.size(), hipMemcpyHostToDevice,
+                                       st)) != hipSuccess ||
+                   (e = launch_border_corr(wp, Kpad, Jpad, C4, d.S, RS, mask_d, mask_d + ncls, (int)ncls, zpx, corr_d,
+                                           st)) != hipSuccess)) ||
         (e = hipStreamSynchronize(st)) != hipSuccess) {
         free_plan(p);
         return hip_fail(e, "conv plan preparation");
@@ -462,9 +706,6 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     a.rounding = d.rnd;
     a.y_ldc = d.y_ldc; a.y_coff = d.y_coff;
     a.vec_store = (d.y_ldc % 4 == 0) && (d.y_coff % 4 == 0);
-    a.tiles_c = tiles_c;
-    a.ntiles = (int)ntiles;
-    p->tile = tile;
     p->avec = gather_width(C4);
     p->mode = d.yt == QNN_INT32 ? OUT_INT32 : OUT_REQUANT;
     a.mode = p->mode;
@@ -473,22 +714,48 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     a.hi_off = hi + off8;
     a.out_xor = off8 ? 0x80808080u : 0u;
     a.staged = p->mode == OUT_REQUANT && env_int("QNN_STAGED", 1) != 0;
+    a.zp4 = 0x01010101u * (uint32_t)(uint8_t)zpx_l;
+    const int32_t *pcorr_tab = pcorr ? corr_d : nullptr;
+    const uint8_t *pcls_tab = pcorr ? pcls_d : nullptr;
+    a.chan_in_lds = (size_t)Kpad * sizeof(ChanRec) <= 64 * 1024;
+    make_divider((uint32_t)Wo, a.mWo, a.sWo);
+    make_divider((uint32_t)Ho, a.mHo, a.sHo);
     p->term3 = term3;
     p->ws_asum_bytes = term3 ? align_up((size_t)M * sizeof(int32_t), 256) : 0;
     p->ws_xpad_bytes = C4 != d.C ? align_up((size_t)d.N * d.H * d.W * C4, 256) : 0;
     p->ws_bytes = p->ws_asum_bytes + p->ws_xpad_bytes;
-    // persistent grid: as many workgroups as stay resident, a multiple of 8
-    // (one share per XCD), never more than there are tiles (rounded up)
-    a.chan_in_lds = (size_t)Kpad * sizeof(ChanRec) <= 64 * 1024;
-    const size_t dyn = a.chan_in_lds ? (size_t)Kpad * sizeof(ChanRec) : 0;
-    const int64_t resident = (int64_t)device_cus() * conv_blocks_per_cu(tile, p->avec, dyn);
-    const int64_t grid = std::min<int64_t>((ntiles + 7) / 8 * 8, std::max<int64_t>(8, resident / 8 * 8));
-    a.nblocks = (int)grid;
-    char buf[160];
-    snprintf(buf, sizeof buf,
-             "conv_mfma tile=%dx%dx%d gather=%d tiles=%lld grid=%d term3=%d cpad=%d M=%lld K=%d J=%lld",
-             ts.tc, ts.tp, ts.bk, p->avec, (long long)ntiles, a.nblocks, (int)term3, C4 != d.C, (long long)M,
-             d.K, (long long)Jg);
+
+    // kernel choice: the candidates are timed on this very shape (the
+    // weights and tables are real, the activations a constant fill) and
+    // the fastest is kept; every candidate computes the same bytes
+    ConvKernel best = cands[0];
+    if (cands.size() > 1 && M > 0 && env_int("QNN_AUTOTUNE", 1) != 0) {
+        if ((s = autotune_conv(a, cands, p->avec, term3, pcorr_tab, pcls_tab, st, &best)) != QNN_OK) {
+            free_plan(p);
+            return s;
+        }
+    }
+    p->ker = best;
+    set_tiling(a, best, p->avec, pcorr_tab, pcls_tab);
+    if ((int64_t)a.ntiles < 0) {
+        free_plan(p);
+        return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
+    }
+    const TileShape ts = kernel_shape(best);
+    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma"};
+    char buf[200];
+    if (best.fam == FAM_GATHER)
+        snprintf(buf, sizeof buf,
+                 "conv_mfma tile=%dx%dx%d gather=%d tiles=%d grid=%d term3=%d cpad=%d M=%lld K=%d J=%lld cands=%d",
+                 ts.tc, ts.tp, ts.bk, p->avec, a.ntiles, a.nblocks, (int)term3, C4 != d.C, (long long)M, d.K,
+                 (long long)Jg, (int)cands.size());
+    else
+        snprintf(buf, sizeof buf,
+                 "%s tile=%dx%dx%d threads=%d stages=%d tiles=%d term3=%d border=%d M=%lld K=%d J=%lld cands=%d",
+                 fam_name[best.fam], ts.tc, ts.tp, ts.bk,
+                 best.fam == FAM_DMA ? dma_threads(best.tile) : tap_threads(best.tile),
+                 best.fam == FAM_DMA ? dma_stages(best.tile) : 2, a.ntiles, (int)term3, (int)ncls, (long long)M, d.K,
+                 (long long)Jg, (int)cands.size());
     p->desc = buf;
     *out = p;
     return QNN_OK;
@@ -534,7 +801,7 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
             a.staged = 0;
         if (p->term3 && (e = launch_window_sums(a, (int32_t *)a.asum, st)) != hipSuccess)
             return hip_fail(e, "window-sum launch");
-        if ((e = launch_conv(a, p->tile, p->avec, st)) != hipSuccess)
+        if ((e = launch_conv_kernel(a, p->ker, p->avec, st)) != hipSuccess)
             return hip_fail(e, "conv launch");
         return QNN_OK;
     }

@@ -36,7 +36,7 @@ struct ConvArgs {
     void *y;                // output (requantized bytes or int32)
     int32_t N, H, W, C, Ho, Wo, R, S;
     int32_t sh, sw, pt, pl, dh, dw;
-    int32_t K, Kpad, J, Jpad, M;
+    int32_t K, Kpad, J, Jpad, M;  // Kpad, Jpad: packed weight rows / row stride
     uint32_t flip4;         // 0x80808080 when x is uint8 (legalised to int8), else 0
     int32_t ydt;            // 0 uint8, 1 int8 (OUT_REQUANT)
     int32_t lo, hi, zp_y, rounding;
@@ -45,12 +45,18 @@ struct ConvArgs {
     int32_t tiles_c;        // channel tiles
     int32_t ntiles;         // tiles_c * pixel tiles
     int32_t nblocks;        // persistent grid size (a multiple of 8)
+    int32_t nk;             // K-steps per tile: ceil(J / BK) of the launched kernel
     int32_t mode;           // OutMode of the conv kernel's epilogue
     int32_t fast_rq;        // 1: HALF_UP and every shift in [33, 53] (32-bit requantize)
     int32_t lo_off, hi_off; // output clamp + off (32-bit requantize path)
     uint32_t out_xor;       // 0x80808080 for int8 outputs of the 32-bit path, else 0
     int32_t staged;         // 1: 8-bit output staged through LDS, 16-byte row stores
     int32_t chan_in_lds;    // 1: chan table copied to dynamic LDS (Kpad * 16 bytes)
+    uint32_t zp4;           // legalised zp_x in all four bytes (padding value of x')
+    // gathers that read zeros for taps outside the image (conv_dma.hip):
+    const uint8_t *pcls;    // [M] border class of each output pixel, 255 = interior
+    const int32_t *pcorr;   // [classes][Kpad] zp_x * weights of the class's outside taps, or nullptr
+    uint32_t mWo, sWo, mHo, sHo;  // magic divisors for m / Wo and t / Ho (mul 0: divisor 1)
 };
 
 // Depthwise conv arguments (channel multiplier 1).
@@ -106,6 +112,57 @@ struct TileShape {
     int tc, tp, bk;
 };
 TileShape tile_shape(int tile);
+
+// Tile configurations of the tap-uniform kernel (conv_tap.hip), used when
+// the channel count is a multiple of the K-step: channels x pixels x BK.
+enum TapTile {
+    TAP_128x128x64 = 0,   // 2x2 waves of 64x64
+    TAP_256x128x64 = 1,   // 4x2 waves of 64x64 (512 threads)
+    TAP_128x256x64 = 2,   // 2x4 waves of 64x64 (512 threads)
+    TAP_128x128x128 = 3,  // 2x2 waves of 64x64
+    TAP_256x128x128 = 4,  // 4x2 waves of 64x64 (512 threads)
+    TAP_128x256x128 = 5,  // 2x4 waves of 64x64 (512 threads)
+    TAP_64x128x128 = 6,   // 1x4 waves of 64x32
+    TAP_128x64x128 = 7,   // 4x1 waves of 32x64
+    TAP_256x128x128_W4 = 8,  // 2x2 waves of 128x64 (one workgroup per CU)
+    TAP_128x256x128_W4 = 9,  // 2x2 waves of 64x128
+    TAP_256x128x64_W4 = 10,  // 2x2 waves of 128x64
+    TAP_128x256x64_W4 = 11,  // 2x2 waves of 64x128
+    TAP_COUNT
+};
+TileShape tap_tile_shape(int tile);
+
+// Tile configurations of the LDS-direct kernel (conv_dma.hip): channels x
+// pixels, wave grid, LDS stages; K-step 64, C % 64 == 0.
+enum DmaTile {
+    DMA_128x128_S4 = 0,   // 2x2 waves of 64x64, 4 stages
+    DMA_128x128_S8 = 1,   // 2x2 waves of 64x64, 8 stages
+    DMA_128x64_S4 = 2,    // 2x2 waves of 64x32
+    DMA_64x128_S4 = 3,    // 2x2 waves of 32x64
+    DMA_64x64_S4 = 4,     // 2x2 waves of 32x32
+    DMA_256x128_S4 = 5,   // 4x2 waves of 64x64 (512 threads)
+    DMA_128x256_S4 = 6,   // 2x4 waves of 64x64 (512 threads)
+    DMA_128x64_S8 = 7,    // 2x2 waves of 64x32, 8 stages
+    DMA_256x128_W4 = 8,   // 2x2 waves of 128x64, 4 stages (one workgroup per CU)
+    DMA_128x256_W4 = 9,   // 2x2 waves of 64x128, 4 stages
+    DMA_128x128_W2A = 10, // 1x2 waves of 128x64, 8 stages
+    DMA_128x128_W2B = 11, // 2x1 waves of 64x128, 8 stages
+    DMA_64x64_S8 = 12,    // 2x2 waves of 32x32, 8 stages
+    DMA_64x128_S8 = 13,   // 2x2 waves of 32x64, 8 stages
+    DMA_64x64_S16 = 14,   // 2x2 waves of 32x32, 16 stages (one workgroup per CU)
+    DMA_COUNT
+};
+TileShape dma_tile_shape(int tile);
+int dma_threads(int tile);
+int dma_stages(int tile);
+hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
+// corr[c][k] = zp_x * (sum of packed weights of row k over the taps outside
+// the image in border class c: tap (r, s) is inside when bit r of rmask[c]
+// and bit s of cmask[c] are set).
+hipError_t launch_border_corr(const int8_t *wp, int Kpad, int Jpad, int C4, int S, int RS, const uint32_t *rmask,
+                              const uint32_t *cmask, int ncls, int32_t zpx, int32_t *corr, hipStream_t st);
+int tap_threads(int tile);
+hipError_t launch_conv_tap(const ConvArgs &a, int tile, hipStream_t st);
 
 // Activation gather width in bytes: 16 when C % 16 == 0, 8 when C % 8 == 0,
 // else 4 (C % 4 == 0 after channel padding).

@@ -23,6 +23,8 @@ import os
 import re
 
 _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
+_TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
+_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false)>")
 
 
 def group_of(kernel_name):
@@ -31,6 +33,14 @@ def group_of(kernel_name):
     if m:
         tc, tp, bk, _, _, avec, _ = (int(v) for v in m.groups())
         return f"conv_mfma tile={tc}x{tp}x{bk} gather={avec}"
+    m = _TAP.search(kernel_name)
+    if m:
+        tc, tp, bk, wc, wp = (int(v) for v in m.groups())
+        return f"conv_tap tile={tc}x{tp}x{bk} threads={wc * wp * 64} stages=2"
+    m = _DMA.search(kernel_name)
+    if m:
+        tc, tp, wc, wp, ns = (int(v) for v in m.groups()[:5])
+        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * 64} stages={ns}"
     base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
     return base
 

@@ -300,3 +300,81 @@ def test_channel_slice_partial_chunk(staged):
     y = out.cpu().numpy()
     assert (y[..., :16] == 201).all() and (y[..., 36:] == 201).all()
     assert_equal(y[..., 16:36], run_oracle(c), f"slice staged={staged}")
+
+
+# The tap-uniform kernels (C % 64 == 0): every configuration of the
+# LDS-direct family (DmaTile) and of the register-staged family (TapTile),
+# forced, on shapes with ragged channel and pixel tiles, padding on every
+# side (the border-class correction), strides, int8 activations (no flip),
+# zero points of 0 (no correction), weight zero points (term 3) and int32
+# outputs.
+TAP_SHAPES = [
+    (W.ConvLayer("t", 23, 21, 64, 200, 3, 3, 1, (1, 1, 1, 1)), 2, {}),
+    (W.ConvLayer("t", 23, 21, 64, 200, 3, 3, 1, (1, 1, 1, 1)), 2, dict(zp_w="channel")),
+    (W.ConvLayer("t", 23, 21, 64, 200, 3, 3, 1, (1, 1, 1, 1)), 2, dict(yt="i32")),
+    (W.ConvLayer("t", 16, 15, 128, 96, 3, 3, 2, (0, 0, 1, 1)), 3, dict(x_dtype="i8")),
+    (W.ConvLayer("t", 17, 17, 128, 72, 1, 7, 1, (0, 3, 0, 3)), 2, dict(rounding="half_away")),
+    (W.ConvLayer("t", 9, 9, 256, 300, 1, 1), 5, dict(yt="i8")),
+    (W.ConvLayer("t", 40, 40, 64, 96, 3, 3, 1, (1, 1, 1, 1)), 8, {}),
+]
+
+
+@pytest.mark.parametrize("tile", list(range(15)))
+def test_every_dma_tile(tile):
+    with env(QNN_DMA=tile):
+        for i, (layer, N, kw) in enumerate(TAP_SHAPES):
+            c = W.conv_case(layer, N, seed=100 + tile * 10 + i, **kw)
+            p, keep = make_plan(c)
+            assert p.describe().startswith("conv_dma"), p.describe()
+            p.close()
+            log(f"dma tile {tile} shape {i}")
+            assert_equal(run_gpu(c), run_oracle(c), f"dma tile {tile} shape {i} {kw}")
+        # zero point 0: no padding correction table
+        c = W.conv_case(TAP_SHAPES[0][0], 2, seed=7)
+        c.zp_x = 0
+        assert_equal(run_gpu(c), run_oracle(c), f"dma tile {tile} zp_x 0")
+
+
+@pytest.mark.parametrize("tile", list(range(12)))
+def test_every_tap_tile(tile):
+    with env(QNN_TAP=tile):
+        for i, (layer, N, kw) in enumerate(TAP_SHAPES):
+            c = W.conv_case(layer, N, seed=200 + tile * 10 + i, **kw)
+            p, keep = make_plan(c)
+            d = p.describe()
+            p.close()
+            if not d.startswith("conv_tap"):
+                continue   # K-step of this tile does not divide the channel count
+            log(f"tap tile {tile} shape {i}")
+            assert_equal(run_gpu(c), run_oracle(c), f"tap tile {tile} shape {i} {kw}")
+
+
+@pytest.mark.parametrize("C,forced", [(64, "dma"), (128, "tap"), (20, "gather"), (64, "auto")])
+def test_dilation(C, forced):
+    """Dilated taps (Eq. (2) with the tap index scaled by the dilation)."""
+    layer = W.ConvLayer("dil", 15, 13, C, 40, 3, 3, 1, (2, 1, 2, 3))
+    c = W.conv_case(layer, 2, seed=C)
+    cfg = {"dma": dict(QNN_DMA=0), "tap": dict(QNN_TAP=3), "gather": {}, "auto": {}}[forced]
+    w, b = dev(c.w), dev(c.bias)
+    with env(**cfg):
+        p = Q.conv2d_plan(c.x.shape, "u8", c.s_x, c.zp_x, w, c.s_w, c.zp_w, b, 1, c.pads, (2, 2), c.s_y, c.zp_y,
+                          c.yt, c.act, c.rounding)
+    y = p.run(dev(c.x))
+    torch.cuda.synchronize()
+    log(f"dilation C={C} {forced}: {p.describe()}")
+    p.close()
+    ref = O.conv2d(c.x, c.s_x, c.zp_x, c.w, c.s_w, c.zp_w, c.bias, c.s_y, c.zp_y, c.yt, c.act, c.rounding,
+                   (1, 1), c.pads, (2, 2))
+    assert_equal(y.cpu().numpy(), ref, f"dilation C={C} {forced}")
+
+
+def test_autotuned_choice_is_a_candidate_and_exact():
+    """Default plans time several kernels on their own shape and keep one;
+    whichever is kept, the bytes are the oracle's."""
+    layer = W.ConvLayer("auto", 28, 28, 128, 128, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 4, seed=5)
+    p, keep = make_plan(c)
+    d = p.describe()
+    p.close()
+    assert "cands=" in d and int(d.split("cands=")[1].split()[0]) > 1, d
+    assert_equal(run_gpu(c), run_oracle(c), d)
