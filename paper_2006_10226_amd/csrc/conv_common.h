@@ -88,7 +88,8 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
     constexpr int WTC = TC / WC, WTP = TP / WP;
     constexpr int FC = WTC / 16, FP = WTP / 16;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
     const int wc = wave / WP, wpos = wave % WP;
     const int lrow = lane & 15, lchk = lane >> 4;
     const int mb = p0 + wpos * WTP + lrow;

@@ -99,7 +99,8 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
     __shared__ __attribute__((aligned(1024))) int8_t lds[LDS_BYTES];
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
     const int wc = wave / WP, wpos = wave % WP;
 
     // XCD x (workgroups dealt round-robin) takes the x-th eighth of the

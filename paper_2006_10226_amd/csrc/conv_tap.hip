@@ -61,7 +61,8 @@ __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>(
     __shared__ __attribute__((aligned(16))) int8_t lds[2 * STAGE];
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
     const int wc = wave / WP, wpos = wave % WP;
 
     // Workgroups are dealt round-robin to the 8 XCDs; XCD x takes the x-th

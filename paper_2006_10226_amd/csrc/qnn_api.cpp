@@ -137,7 +137,7 @@ enum PlanKind { PLAN_CONV = 0, PLAN_DW = 1, PLAN_REQ = 2 };
 }  // namespace
 
 // One implicit-GEMM kernel configuration: family and tile enum value.
-enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2 };
+enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3 };
 struct ConvKernel {
     int fam = FAM_GATHER;
     int tile = TILE_64x64;
@@ -292,6 +292,7 @@ qnn_status read_bias(const int32_t *bias, int n, hipStream_t st, std::vector<int
 TileShape kernel_shape(const ConvKernel &k)
 {
     switch (k.fam) {
+    case FAM_WAVE: return {64, 64, 64};
     case FAM_DMA: return dma_tile_shape(k.tile);
     case FAM_TAP: return tap_tile_shape(k.tile);
     default: return tile_shape(k.tile);
@@ -307,12 +308,19 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
     (void)K;
     std::vector<ConvKernel> c;
     const int f_dma = env_int("QNN_DMA", -1), f_tap = env_int("QNN_TAP", -1), f_tile = env_int("QNN_TILE", -1);
+    const int f_wave = env_int("QNN_WAVE", -1);
+    if ((f_wave == 1 || f_wave == 2 || f_wave == 4) && dma_ok)
+        return {{FAM_WAVE, f_wave}};
     if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok)
         return {{FAM_DMA, f_dma}};
     if (f_tap >= 0 && f_tap < TAP_COUNT && tap_ok && C4 % tap_tile_shape(f_tap).bk == 0)
         return {{FAM_TAP, f_tap}};
     if (f_tile >= 0 && f_tile < TILE_COUNT)
         return {{FAM_GATHER, f_tile}};
+    if (dma_ok && env_int("QNN_WAVE", -1) != -2)
+        for (int sp : {1, 2, 4})
+            if (sp == 1 || J / 64 >= 2 * sp)
+                c.push_back({FAM_WAVE, sp});
     if (dma_ok && env_int("QNN_DMA", -1) != -2)
         for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_256x128_S4, DMA_128x256_S4,
                       DMA_128x128_S8, DMA_128x64_S8, DMA_64x64_S8, DMA_64x128_S8, DMA_64x64_S16})
@@ -335,8 +343,9 @@ int device_cus();
 void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr_tab, const uint8_t *pcls_tab)
 {
     const TileShape ts = kernel_shape(k);
-    a.pcorr = k.fam == FAM_DMA ? pcorr_tab : nullptr;
-    a.pcls = k.fam == FAM_DMA ? pcls_tab : nullptr;
+    const bool zero_pad = k.fam == FAM_DMA || k.fam == FAM_WAVE;   // gathers read x = 0 outside the image
+    a.pcorr = zero_pad ? pcorr_tab : nullptr;
+    a.pcls = zero_pad ? pcls_tab : nullptr;
     const int64_t tiles_c = (a.K + ts.tc - 1) / ts.tc;
     const int64_t ntiles = tiles_c * (((int64_t)a.M + ts.tp - 1) / ts.tp);
     a.tiles_c = (int)tiles_c;
@@ -355,6 +364,7 @@ void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr
 hipError_t launch_conv_kernel(const ConvArgs &a, const ConvKernel &k, int avec, hipStream_t st)
 {
     switch (k.fam) {
+    case FAM_WAVE: return launch_conv_wave(a, k.tile, st);
     case FAM_DMA: return launch_conv_dma(a, k.tile, st);
     case FAM_TAP: return launch_conv_tap(a, k.tile, st);
     default: return launch_conv(a, k.tile, avec, st);
@@ -632,22 +642,25 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
             fast = false;
 
     const size_t wp_bytes = align_up((size_t)Kpad * Jpad, 256);
+    const size_t wf_bytes = dma_ok ? wp_bytes : 0;
     const size_t ch_bytes = align_up(sizeof(ChanRec) * Kpad, 256);
     const size_t zw_bytes = align_up(sizeof(int32_t) * Kpad, 256);
     const size_t pad_bytes = 256;
     const size_t pcls_bytes = pcorr ? align_up((size_t)M, 256) : 0;
     const size_t corr_bytes = pcorr ? align_up(sizeof(int32_t) * ncls * Kpad, 256) : 0;
     const size_t mask_bytes = pcorr ? align_up(sizeof(uint32_t) * 2 * ncls, 256) : 0;
-    const size_t total = wp_bytes + ch_bytes + zw_bytes + pad_bytes + pcls_bytes + corr_bytes + mask_bytes;
+    const size_t total =
+        wp_bytes + wf_bytes + ch_bytes + zw_bytes + pad_bytes + pcls_bytes + corr_bytes + mask_bytes;
     hipError_t e = hipMalloc(&p->dev, total);
     if (e != hipSuccess) {
         free_plan(p);
         return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", total);
     }
     int8_t *wp = (int8_t *)p->dev;
-    ChanRec *chan = (ChanRec *)((char *)p->dev + wp_bytes);
-    int32_t *zpw_d = (int32_t *)((char *)p->dev + wp_bytes + ch_bytes);
-    uint8_t *padbuf = (uint8_t *)p->dev + wp_bytes + ch_bytes + zw_bytes;
+    int8_t *wf = dma_ok ? wp + wp_bytes : nullptr;
+    ChanRec *chan = (ChanRec *)((char *)p->dev + wp_bytes + wf_bytes);
+    int32_t *zpw_d = (int32_t *)((char *)chan + ch_bytes);
+    uint8_t *padbuf = (uint8_t *)zpw_d + zw_bytes;
     // channel records, weight zero points and the padding block (zp_x
     // bytes) in one upload
     std::vector<uint8_t> host(ch_bytes + zw_bytes + pad_bytes, 0);
@@ -678,6 +691,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     if ((e = hipMemcpyAsync(chan, host.data(), host.size(), hipMemcpyHostToDevice, st)) != hipSuccess ||
         (e = launch_prep_conv(d.w, d.bias, d.K, RS, d.C, C4, Jpad, Kpad, zpx_l, wp, chan, zpw_d, st)) !=
             hipSuccess ||
+        (wf && (e = launch_frag_pack(wp, Kpad, Jpad, wf, st)) != hipSuccess) ||
         (pcorr && ((e = hipMemcpyAsync(pcls_d, bc.pcls.data(), (size_t)M, hipMemcpyHostToDevice, st)) != hipSuccess ||
                    (e = hipMemcpyAsync(mask_d, masks.data(), sizeof(uint32_t) * masks.size(), hipMemcpyHostToDevice,
                                        st)) != hipSuccess ||
@@ -690,6 +704,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
 
     ConvArgs &a = p->conv;
     a.wp = wp;
+    a.wf = wf;
     a.chan = chan;
     a.zpw = zpw_d;
     a.padbuf = padbuf;
@@ -742,7 +757,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
     }
     const TileShape ts = kernel_shape(best);
-    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma"};
+    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave"};
     char buf[200];
     if (best.fam == FAM_GATHER)
         snprintf(buf, sizeof buf,
@@ -753,9 +768,13 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         snprintf(buf, sizeof buf,
                  "%s tile=%dx%dx%d threads=%d stages=%d tiles=%d term3=%d border=%d M=%lld K=%d J=%lld cands=%d",
                  fam_name[best.fam], ts.tc, ts.tp, ts.bk,
-                 best.fam == FAM_DMA ? dma_threads(best.tile) : tap_threads(best.tile),
-                 best.fam == FAM_DMA ? dma_stages(best.tile) : 2, a.ntiles, (int)term3, (int)ncls, (long long)M, d.K,
-                 (long long)Jg, (int)cands.size());
+                 best.fam == FAM_DMA ? dma_threads(best.tile) : best.fam == FAM_WAVE ? 256 : tap_threads(best.tile),
+                 best.fam == FAM_DMA ? dma_stages(best.tile) : best.fam == FAM_WAVE ? 4 : 2, a.ntiles, (int)term3,
+                 (int)ncls, (long long)M, d.K, (long long)Jg, (int)cands.size());
+    if (best.fam == FAM_WAVE) {
+        const size_t n = strlen(buf);
+        snprintf(buf + n, sizeof buf - n, " split=%d", best.tile);
+    }
     p->desc = buf;
     *out = p;
     return QNN_OK;

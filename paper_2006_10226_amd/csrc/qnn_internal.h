@@ -29,6 +29,7 @@ enum OutMode { OUT_REQUANT = 0, OUT_INT32 = 1 };
 struct ConvArgs {
     const uint8_t *x;       // NHWC activations (uint8 or int8 bytes)
     const int8_t *wp;       // packed weights [Kpad][Jpad], zero padded
+    const int8_t *wf;       // the same weights in MFMA operand order (conv_wave.hip)
     const ChanRec *chan;    // [Kpad]
     const int32_t *zpw;     // [Kpad] weight zero points (term 3)
     const int32_t *asum;    // [M] window sums of x' (term 3) or nullptr
@@ -156,6 +157,10 @@ TileShape dma_tile_shape(int tile);
 int dma_threads(int tile);
 int dma_stages(int tile);
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
+// Wave-independent kernel (conv_wave.hip): 64 x 64 tile per wave, split =
+// 1, 2 or 4 waves sharing a tile's reduction.
+hipError_t launch_conv_wave(const ConvArgs &a, int split, hipStream_t st);
+hipError_t launch_frag_pack(const int8_t *wp, int Kpad, int Jpad, int8_t *out, hipStream_t st);
 // corr[c][k] = zp_x * (sum of packed weights of row k over the taps outside
 // the image in border class c: tap (r, s) is inside when bit r of rmask[c]
 // and bit s of cmask[c] are set).

@@ -378,3 +378,21 @@ def test_autotuned_choice_is_a_candidate_and_exact():
     p.close()
     assert "cands=" in d and int(d.split("cands=")[1].split()[0]) > 1, d
     assert_equal(run_gpu(c), run_oracle(c), d)
+
+
+@pytest.mark.parametrize("split", [1, 2, 4])
+def test_every_wave_split(split):
+    """The wave-independent kernel with 1, 2 and 4 waves sharing a tile's
+    reduction, forced, on the tap-kernel shapes (ragged tiles, padding,
+    strides, int8 input, term 3, int32 output, odd step counts)."""
+    with env(QNN_WAVE=split):
+        for i, (layer, N, kw) in enumerate(TAP_SHAPES):
+            c = W.conv_case(layer, N, seed=300 + split * 10 + i, **kw)
+            p, keep = make_plan(c)
+            assert p.describe().startswith("conv_wave"), p.describe()
+            p.close()
+            log(f"wave split {split} shape {i}")
+            assert_equal(run_gpu(c), run_oracle(c), f"wave split {split} shape {i} {kw}")
+        c = W.conv_case(TAP_SHAPES[0][0], 2, seed=8)
+        c.zp_x = 0
+        assert_equal(run_gpu(c), run_oracle(c), f"wave split {split} zp_x 0")
