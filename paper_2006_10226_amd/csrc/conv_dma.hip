@@ -138,7 +138,18 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         const int m = p0 + row;
         pbase[i] = 0;
         pmask[i] = 0;
-        if (m < a.M) {
+        if (m < a.M && a.rowpack) {
+            // row-pair mode: K-step s holds filter rows 2s and 2s + 1, each a
+            // 32-byte run of the zero-point-padded image starting at the
+            // window's first tap; logical chunk q: row q / 2, half q % 2
+            const int t = fast_div(m, a.mWo, a.sWo);
+            const int ow = m - t * a.Wo;
+            const int n = fast_div(t, a.mHo, a.sHo);
+            const int oh = t - n * a.Ho;
+            const int q = pch ^ sw64(row);
+            pbase[i] = ((n * a.H + oh * a.sh) * a.W + ow * a.sw) * a.C + (q >> 1) * a.row_bytes + (q & 1) * 16;
+            pmask[i] = 0xffffffffu;
+        } else if (m < a.M) {
             const int t = fast_div(m, a.mWo, a.sWo);
             const int ow = m - t * a.Wo;
             const int n = fast_div(t, a.mHo, a.sHo);
@@ -159,7 +170,7 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
     int lr = 0, ls = 0, lc = 0;
     int voffB[LB];
     auto set_tap = [&]() {
-        const int toff = (lr * a.dh * a.W + ls * a.dw) * a.C;
+        const int toff = a.rowpack ? lr * 2 * a.row_bytes : (lr * a.dh * a.W + ls * a.dw) * a.C;
         const uint32_t rin = lr < a.R ? 1u : 0u;
 #pragma unroll
         for (int i = 0; i < LB; ++i) {
@@ -182,6 +193,11 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
 #pragma unroll
         for (int i = 0; i < LB; ++i)
             dma16(rx, base + TC * BK + (i * NW + wave) * 16 * BK, voffB[i], soffB);
+        if (a.rowpack) {
+            ++lr;   // next row pair; lr == R (pairs) past the end: out of range
+            set_tap();
+            return;
+        }
         lc += BK;
         if (lc == a.C) {
             lc = 0;
@@ -286,6 +302,70 @@ hipError_t launch_border_corr(const int8_t *wp, int Kpad, int Jpad, int C4, int 
     const int n = ncls * Kpad;
     hipLaunchKernelGGL(border_corr_kernel, dim3((n + 255) / 256), dim3(256), 0, st, wp, Kpad, Jpad, C4, S, RS, rmask,
                        cmask, ncls, zpx, corr);
+    return hipGetLastError();
+}
+
+// Row-pair packing of the weights for small channel counts (S * C4 <= 32):
+// wp[k][64 s + 32 h + b] = w[k][r][b / C4][b % C4] for filter row r = 2 s + h,
+// zero where r >= R, b / C4 >= S or b % C4 >= C.  One thread per byte.
+__global__ void __launch_bounds__(256) rowpack_weights_kernel(const int8_t *w, int K, int R, int S, int C, int C4,
+                                                              int Kpad, int Jpad, int8_t *wp)
+{
+    const long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= (long long)Kpad * Jpad)
+        return;
+    const int k = (int)(g / Jpad), j = (int)(g - (long long)k * Jpad);
+    const int s = j >> 6, h = (j >> 5) & 1, b = j & 31;
+    const int r = 2 * s + h, tap = b / C4, c = b - tap * C4;
+    int8_t v = 0;
+    if (k < K && r < R && tap < S && c < C)
+        v = w[(((size_t)k * R + r) * S + tap) * C + c];
+    wp[g] = v;
+}
+
+// Zero-point padded copy of the image for the row-pair mode:
+// out[n][h][w][c] = x[n][h - pt][w - pl][c] inside, zp elsewhere (also in
+// the padded channels c >= C).  One thread per padded pixel (C4 <= 32 bytes,
+// written as whole dwords; C4 is a multiple of 4).
+__global__ void __launch_bounds__(256) pad_image_kernel(const uint8_t *x, int N, int H, int W, int C, int Hp, int Wp,
+                                                        int C4, int pt, int pl, uint8_t zp, uint8_t *out)
+{
+    const long long pix = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (pix >= (long long)N * Hp * Wp)
+        return;
+    const int w = (int)(pix % Wp);
+    const long long t = pix / Wp;
+    const int h = (int)(t % Hp), n = (int)(t / Hp);
+    const int ih = h - pt, iw = w - pl;
+    const bool in = (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
+    const uint8_t *src = x + (((size_t)n * H + (in ? ih : 0)) * W + (in ? iw : 0)) * C;
+    uint32_t *dst = (uint32_t *)(out + pix * C4);
+    for (int c0 = 0; c0 < C4; c0 += 4) {
+        uint32_t v = 0;
+        for (int e = 0; e < 4; ++e) {
+            const int c = c0 + e;
+            const uint32_t b = (in && c < C) ? src[c] : zp;
+            v |= b << (8 * e);
+        }
+        dst[c0 >> 2] = v;
+    }
+}
+
+hipError_t launch_rowpack_weights(const int8_t *w, int K, int R, int S, int C, int C4, int Kpad, int Jpad, int8_t *wp,
+                                  hipStream_t st)
+{
+    const long long n = (long long)Kpad * Jpad;
+    hipLaunchKernelGGL(rowpack_weights_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, w, K, R, S, C, C4,
+                       Kpad, Jpad, wp);
+    return hipGetLastError();
+}
+
+hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp, int Wp, int C4, int pt, int pl,
+                            uint8_t zp, uint8_t *out, hipStream_t st)
+{
+    const long long n = (long long)N * Hp * Wp;
+    hipLaunchKernelGGL(pad_image_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, x, N, H, W, C, Hp, Wp,
+                       C4, pt, pl, zp, out);
     return hipGetLastError();
 }
 

@@ -152,6 +152,8 @@ struct qnn_plan {
     bool term3 = false;
     size_t ws_asum_bytes = 0, ws_xpad_bytes = 0;
     int32_t C_in = 0;           // channels of the caller's x (before padding to a.C)
+    bool rowpack = false;       // row-pair mode: x is copied into a zero-point padded image
+    int32_t H_in = 0, W_in = 0, pt_in = 0, pl_in = 0;   // caller's image and pads (row-pair mode)
     uint8_t pad_zp = 0;         // zero point byte written into padded channels
     // depthwise
     DwArgs dw{};
@@ -620,17 +622,41 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     // the tap kernels gather one filter tap per K-step (C4 % BK == 0); the
     // LDS-direct one also needs the border classes for its padding fix-up
     BorderClasses bc;
-    const bool tap_ok = C4 % 64 == 0 && d.R <= 16 && d.S <= 16;
-    const bool dma_ok = tap_ok && border_classes(d, Ho, Wo, M, bc);
-    const bool pcorr = dma_ok && bc.any && zpx != 0;
-    const size_t ncls = pcorr ? bc.rmask.size() : 0;
-    const std::vector<ConvKernel> cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok);
     const bool term3 = [&] {
         for (int i = 0; i < d.wq.n; ++i)
             if (d.wq.zero_point[i] != 0)
                 return true;
         return false;
     }();
+    const bool tap_ok = C4 % 64 == 0 && d.R <= 16 && d.S <= 16;
+    // row-pair mode of the LDS-direct kernel for small channel counts (the
+    // 3-channel stems): two filter rows of S * C4 <= 32 bytes per K-step,
+    // over a zero-point padded copy of the image
+    const bool rowpack = !tap_ok && C4 * d.S <= 32 && d.R <= 32 && d.cp.dil_h == 1 && d.cp.dil_w == 1 && !term3 &&
+                         env_int("QNN_ROWPACK", 1) != 0 && env_int("QNN_TILE", -1) < 0;
+    const int npairs = (d.R + 1) / 2;
+    const int Jr = npairs * 64;                      // row-pair reduction length
+    const int Hp = std::max(d.H + d.cp.pad_top + d.cp.pad_bottom, (Ho - 1) * d.cp.stride_h + 2 * npairs);
+    const int Wp = std::max(d.W + d.cp.pad_left + d.cp.pad_right, (Wo - 1) * d.cp.stride_w + (32 + C4 - 1) / C4);
+    if (rowpack && (int64_t)d.N * Hp * Wp * C4 >= (int64_t(1) << 31)) {
+        free_plan(p);
+        return fail(QNN_ERR_UNSUPPORTED, "padded image of 2^31 bytes or more");
+    }
+    const bool dma_ok = tap_ok && border_classes(d, Ho, Wo, M, bc);
+    const bool pcorr = dma_ok && bc.any && zpx != 0;
+    const size_t ncls = pcorr ? bc.rmask.size() : 0;
+    std::vector<ConvKernel> cands;
+    if (rowpack) {
+        const int f = env_int("QNN_DMA", -1);
+        if (f >= 0 && f < DMA_COUNT)
+            cands.push_back({FAM_DMA, f});
+        else
+            for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_128x64_S8, DMA_64x128_S8,
+                          DMA_64x64_S8})
+                cands.push_back({FAM_DMA, t});
+    } else {
+        cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok);
+    }
     // legalisation (Sec. III-C): uint8 activations become int8 by x - 128
     const int32_t zpx_l = d.xt == QNN_UINT8 ? zpx - 128 : zpx;
     // 32-bit requantize in the epilogue when every channel allows it
@@ -643,6 +669,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
 
     const size_t wp_bytes = align_up((size_t)Kpad * Jpad, 256);
     const size_t wf_bytes = dma_ok ? wp_bytes : 0;
+    const size_t wr_bytes = rowpack ? align_up((size_t)Kpad * Jr, 256) : 0;
     const size_t ch_bytes = align_up(sizeof(ChanRec) * Kpad, 256);
     const size_t zw_bytes = align_up(sizeof(int32_t) * Kpad, 256);
     const size_t pad_bytes = 256;
@@ -650,7 +677,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     const size_t corr_bytes = pcorr ? align_up(sizeof(int32_t) * ncls * Kpad, 256) : 0;
     const size_t mask_bytes = pcorr ? align_up(sizeof(uint32_t) * 2 * ncls, 256) : 0;
     const size_t total =
-        wp_bytes + wf_bytes + ch_bytes + zw_bytes + pad_bytes + pcls_bytes + corr_bytes + mask_bytes;
+        wp_bytes + wf_bytes + wr_bytes + ch_bytes + zw_bytes + pad_bytes + pcls_bytes + corr_bytes + mask_bytes;
     hipError_t e = hipMalloc(&p->dev, total);
     if (e != hipSuccess) {
         free_plan(p);
@@ -658,7 +685,8 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     }
     int8_t *wp = (int8_t *)p->dev;
     int8_t *wf = dma_ok ? wp + wp_bytes : nullptr;
-    ChanRec *chan = (ChanRec *)((char *)p->dev + wp_bytes + wf_bytes);
+    int8_t *wr = rowpack ? wp + wp_bytes + wf_bytes : nullptr;
+    ChanRec *chan = (ChanRec *)((char *)p->dev + wp_bytes + wf_bytes + wr_bytes);
     int32_t *zpw_d = (int32_t *)((char *)chan + ch_bytes);
     uint8_t *padbuf = (uint8_t *)zpw_d + zw_bytes;
     // channel records, weight zero points and the padding block (zp_x
@@ -692,6 +720,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         (e = launch_prep_conv(d.w, d.bias, d.K, RS, d.C, C4, Jpad, Kpad, zpx_l, wp, chan, zpw_d, st)) !=
             hipSuccess ||
         (wf && (e = launch_frag_pack(wp, Kpad, Jpad, wf, st)) != hipSuccess) ||
+        (wr && (e = launch_rowpack_weights(d.w, d.K, d.R, d.S, d.C, C4, Kpad, Jr, wr, st)) != hipSuccess) ||
         (pcorr && ((e = hipMemcpyAsync(pcls_d, bc.pcls.data(), (size_t)M, hipMemcpyHostToDevice, st)) != hipSuccess ||
                    (e = hipMemcpyAsync(mask_d, masks.data(), sizeof(uint32_t) * masks.size(), hipMemcpyHostToDevice,
                                        st)) != hipSuccess ||
@@ -737,7 +766,21 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     make_divider((uint32_t)Ho, a.mHo, a.sHo);
     p->term3 = term3;
     p->ws_asum_bytes = term3 ? align_up((size_t)M * sizeof(int32_t), 256) : 0;
-    p->ws_xpad_bytes = C4 != d.C ? align_up((size_t)d.N * d.H * d.W * C4, 256) : 0;
+    p->ws_xpad_bytes = rowpack ? align_up((size_t)d.N * Hp * Wp * C4, 256)
+                               : C4 != d.C ? align_up((size_t)d.N * d.H * d.W * C4, 256) : 0;
+    p->rowpack = rowpack;
+    p->H_in = d.H; p->W_in = d.W; p->pt_in = d.cp.pad_top; p->pl_in = d.cp.pad_left;
+    if (rowpack) {
+        // the kernel sees the padded image, unpadded, with row pairs as taps
+        a.wp = wr;
+        a.Jpad = Jr;
+        a.J = Jr;
+        a.H = Hp; a.W = Wp;
+        a.pt = 0; a.pl = 0;
+        a.R = npairs; a.S = 1;
+        a.rowpack = 1;
+        a.row_bytes = Wp * C4;
+    }
     p->ws_bytes = p->ws_asum_bytes + p->ws_xpad_bytes;
 
     // kernel choice: the candidates are timed on this very shape (the
@@ -801,9 +844,15 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
         hipError_t e;
         if (p->ws_xpad_bytes) {
             uint8_t *xp = (uint8_t *)ws + p->ws_asum_bytes;
-            const long long pixels = (long long)a.N * a.H * a.W;
-            if ((e = launch_pad_channels(a.x, xp, pixels, p->C_in, a.C, p->pad_zp, st)) != hipSuccess)
-                return hip_fail(e, "channel padding launch");
+            if (p->rowpack) {
+                if ((e = launch_pad_image(a.x, a.N, p->H_in, p->W_in, p->C_in, a.H, a.W, a.C, p->pt_in, p->pl_in,
+                                          p->pad_zp, xp, st)) != hipSuccess)
+                    return hip_fail(e, "image padding launch");
+            } else {
+                const long long pixels = (long long)a.N * a.H * a.W;
+                if ((e = launch_pad_channels(a.x, xp, pixels, p->C_in, a.C, p->pad_zp, st)) != hipSuccess)
+                    return hip_fail(e, "channel padding launch");
+            }
             a.x = xp;
             x = xp;
         }

@@ -58,6 +58,10 @@ struct ConvArgs {
     const uint8_t *pcls;    // [M] border class of each output pixel, 255 = interior
     const int32_t *pcorr;   // [classes][Kpad] zp_x * weights of the class's outside taps, or nullptr
     uint32_t mWo, sWo, mHo, sHo;  // magic divisors for m / Wo and t / Ho (mul 0: divisor 1)
+    // row-pair mode of conv_dma.hip (S * C4 <= 32): x is the zero-point
+    // padded image (H, W padded, pads 0), R counts filter row pairs, S is 1,
+    // and row_bytes is the padded image's row stride
+    int32_t rowpack, row_bytes;
 };
 
 // Depthwise conv arguments (channel multiplier 1).
@@ -164,6 +168,10 @@ hipError_t launch_frag_pack(const int8_t *wp, int Kpad, int Jpad, int8_t *out, h
 // corr[c][k] = zp_x * (sum of packed weights of row k over the taps outside
 // the image in border class c: tap (r, s) is inside when bit r of rmask[c]
 // and bit s of cmask[c] are set).
+hipError_t launch_rowpack_weights(const int8_t *w, int K, int R, int S, int C, int C4, int Kpad, int Jpad, int8_t *wp,
+                                  hipStream_t st);
+hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp, int Wp, int C4, int pt, int pl,
+                            uint8_t zp, uint8_t *out, hipStream_t st);
 hipError_t launch_border_corr(const int8_t *wp, int Kpad, int Jpad, int C4, int S, int RS, const uint32_t *rmask,
                               const uint32_t *cmask, int ncls, int32_t zpx, int32_t *corr, hipStream_t st);
 int tap_threads(int tile);

@@ -396,3 +396,28 @@ def test_every_wave_split(split):
         c = W.conv_case(TAP_SHAPES[0][0], 2, seed=8)
         c.zp_x = 0
         assert_equal(run_gpu(c), run_oracle(c), f"wave split {split} zp_x 0")
+
+
+@pytest.mark.parametrize("layer,N", [
+    (W.ConvLayer("stem", 29, 31, 3, 64, 7, 7, 2, (3, 3, 3, 3)), 3),
+    (W.ConvLayer("stem3", 35, 33, 3, 32, 3, 3, 2, (0, 0, 0, 0)), 2),
+    (W.ConvLayer("stem3p", 20, 20, 3, 40, 3, 3, 1, (1, 2, 0, 1)), 2),
+    (W.ConvLayer("c8", 17, 16, 8, 24, 3, 3, 1, (1, 1, 1, 1)), 2),
+    (W.ConvLayer("c4_5x5", 15, 15, 4, 70, 5, 5, 2, (2, 2, 2, 2)), 2),
+])
+def test_row_pair_mode(layer, N):
+    """Small channel counts (S * C4 <= 32) through the row-pair mode of the
+    LDS-direct kernel (zero-point padded image, two filter rows per
+    K-step), for every configuration the plan may pick."""
+    for tile in (None, 0, 3, 4, 12):
+        cfg = {} if tile is None else dict(QNN_DMA=tile)
+        for kw in ({}, dict(x_dtype="i8", yt="i8")):
+            c = W.conv_case(layer, N, seed=17, **kw)
+            with env(**cfg):
+                p, keep = make_plan(c)
+            d = p.describe()
+            p.close()
+            assert d.startswith("conv_dma"), d
+            with env(**cfg):
+                got = run_gpu(c)
+            assert_equal(got, run_oracle(c), f"{layer.name} tile {tile} {kw}: {d}")
