@@ -139,6 +139,8 @@ def kernel_group(it):
     words = it.desc.split()
     d = dict(kv.split("=") for kv in words[1:] if "=" in kv)
     extra = f"gather={d['gather']}" if "gather" in d else f"threads={d['threads']} stages={d.get('stages', '')}"
+    if "split" in d:
+        extra += f" split={d['split']}"
     return f"{words[0]} tile={d['tile']} {extra}"
 
 
@@ -247,14 +249,13 @@ def traffic_for(group):
     """HBM bytes per launch of the dominant kernel from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary, if it was taken on the current
     kernel source (else None)."""
-    import hashlib
+    from paper_2006_10226_amd.rocprof_summary import kernel_source_sha1
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     try:
         rec = json.load(open(path))
-        src = open(os.path.join(ROOT, "paper_2006_10226_amd", "csrc", "conv_mfma.hip"), "rb").read()
-        if rec.get("source_sha1") != hashlib.sha1(src).hexdigest():
+        if rec.get("source_sha1") != kernel_source_sha1(ROOT):
             return None
         return rec.get("groups", {}).get(group, {}).get("bytes_per_launch")
     except Exception:
@@ -273,6 +274,8 @@ def main():
                     help="only run a plain device-to-device copy of MIB MiB (3 times), for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters, and exit")
     ap.add_argument("--layers-out", default=None, help="write per-layer timings as JSON to this file")
+    ap.add_argument("--tuning-file", default=None,
+                    help="kernel-choice file: reuse the choices recorded there, append newly timed ones")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -291,6 +294,9 @@ def main():
         torch.cuda.synchronize()
         log(f"copied {n} bytes 3 times")
         return
+    if args.tuning_file:
+        from paper_2006_10226_amd import qnn
+        qnn.set_tuning_file(args.tuning_file)
     log(f"setting up {args.workload}")
     items, batch = setup(args.workload)
     total_macs = sum(it.macs for it in items)
@@ -313,7 +319,8 @@ def main():
     dom = max(groups, key=lambda g: groups[g]["ms"])
     D = groups[dom]
     avg_ms = D["ms"] / D["launches"]
-    if D["macs"] > 0:
+    if D["macs"] > 0 and dom.startswith("conv_"):
+        # conv and dense run on the matrix cores
         achieved = 2.0 * D["macs"] / D["launches"] / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": round(achieved / PEAK_INT8_TOPS, 4)}

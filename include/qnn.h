@@ -209,7 +209,9 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
  * derives the per-channel fixed-point multipliers and the folded constant
  * bias[k] - zp_x*sum_j w[k,j] + J*zp_x*zp_w[k], and packs the weights into
  * device memory it owns.  Arguments mean what they mean in the one-shot
- * calls; x and y are given at run time.  Creation synchronizes `stream`.
+ * calls; x and y are given at run time.  Creation synchronizes `stream`;
+ * conv and dense creation also times the candidate kernels on `stream`
+ * (see qnn_set_tuning_file), using scratch device memory it frees again.
  * A plan is immutable after creation: runs on different streams may overlap
  * provided each passes its own workspace (see qnn_plan_workspace_size).
  */
@@ -256,9 +258,24 @@ qnn_status qnn_plan_run(const qnn_plan *plan, void *stream, const void *x, void 
 /* Bytes of device workspace a run needs (0 if none). */
 size_t qnn_plan_workspace_size(const qnn_plan *plan);
 
-/* Human-readable kernel choice of the plan, e.g. "conv_mfma 128x128x128
- * split1"; valid until the plan is destroyed. */
+/* Human-readable kernel choice of the plan, e.g. "conv_dma tile=128x128x64
+ * threads=256 stages=4 ..."; valid until the plan is destroyed. */
 const char *qnn_plan_describe(const qnn_plan *plan);
+
+/*
+ * Kernel-choice file.  A conv or dense plan picks its kernel by timing the
+ * eligible candidate kernels on its own shape at creation (each candidate
+ * computes the same bytes; only the time differs).  After this call with a
+ * path, creation first looks its shape up in the file's records and, when
+ * the recorded choice is still a candidate, takes it without timing; a
+ * choice it does time is appended to the file as one text line,
+ * "<shape key> <family> <config>".  A missing file starts empty.  NULL or
+ * "" stops reading and writing any file and forgets the records.  Returns
+ * QNN_ERR_UNSUPPORTED when the file exists but cannot be read.  Plans
+ * created concurrently with this call see either the old or the new
+ * records.
+ */
+qnn_status qnn_set_tuning_file(const char *path);
 
 /* Frees the plan's device memory (after synchronizing the device). NULL is
  * a no-op. */

@@ -27,6 +27,8 @@
 //     and the epilogue adds it (store_tile).
 #include "conv_common.h"
 
+#include <type_traits>
+
 namespace qnn {
 
 using namespace conv;
@@ -79,7 +81,11 @@ constexpr int dma_occupancy()
     return WTC * WTP >= 128 * 64 ? 1 : 2;
 }
 
-template <int TC, int TP, int WC, int WP, int NS, bool FLIP>
+// SHORT: reductions of at most NS K-steps (1x1 convolutions with few input
+// channels).  All NS stages are issued at once into their own buffers (no
+// ring), so the LDS footprint is only NS stages and more workgroups stay
+// resident to cover the memory latency of these one-pass tiles.
+template <int TC, int TP, int WC, int WP, int NS, bool FLIP, bool SHORT>
 __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>())) conv_dma_kernel(ConvArgs a)
 {
     constexpr int NW = WC * WP;
@@ -92,9 +98,9 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
     constexpr int LPS = LA + LB;         // loads per lane per stage
     constexpr int LDS_BYTES = NS * STAGE > TP * (TC + 16) ? NS * STAGE : TP * (TC + 16);
     static_assert(TC % (16 * NW) == 0 && TP % (16 * NW) == 0, "every wave loads whole 16-row blocks");
-    static_assert((NS & (NS - 1)) == 0 && NS >= 2, "stage count is a power of two");
-    static_assert(LPS * (NS - 2) < 64, "vmcnt range");
-    static_assert(NS >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
+    static_assert((NS & (NS - 1)) == 0, "stage count is a power of two");
+    static_assert(LPS * (SHORT ? NS - 1 : NS - 2) < 64, "vmcnt range");
+    static_assert(SHORT || NS >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
 
     __shared__ __attribute__((aligned(1024))) int8_t lds[LDS_BYTES];
 
@@ -242,34 +248,60 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
                 acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[i], B[j], acc[i][j], 0, 0, 0);
     };
 
-    // ---- pipeline ---------------------------------------------------------
-    // NS - 1 stages of loads in flight; the fragments of stage k + 1 are
-    // read from LDS while the MFMAs of stage k run.  The barrier of step k
-    // certifies that stage k + 1 has landed everywhere and that every wave
-    // is done with step k - 1, so buffer (k - 1) mod NS takes stage
-    // k + NS - 1.
-    set_tap();
+    if constexpr (SHORT) {
+        // every stage in flight at once; stage k is read as soon as it (and
+        // the stages before it) have landed in every wave
+        set_tap();
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-        issue(s);
-    stage_barrier<LPS *(NS - 2)>();
-    read_frags(0, fa[0], fb[0]);
-    int k = 0;
-    for (; k + 2 <= nk; k += 2) {
-        stage_barrier<LPS *(NS - 3)>();
-        issue(k + NS - 1);
-        read_frags(k + 1, fa[1], fb[1]);
-        mfma(fa[0], fb[0]);
-        stage_barrier<LPS *(NS - 3)>();
-        issue(k + NS);
-        read_frags(k + 2, fa[0], fb[0]);
-        mfma(fa[1], fb[1]);
+        for (int s = 0; s < NS; ++s)
+            issue(s);
+        auto step = [&](auto S) __attribute__((always_inline)) {
+            constexpr int k = decltype(S)::value;
+            if constexpr (k < NS) {
+                stage_barrier<LPS *(NS - 1 - k)>();
+                if (k < nk) {
+                    read_frags(k, fa[0], fb[0]);
+                    mfma(fa[0], fb[0]);
+                }
+            }
+        };
+        step(std::integral_constant<int, 0>{});
+        step(std::integral_constant<int, 1>{});
+        step(std::integral_constant<int, 2>{});
+        step(std::integral_constant<int, 3>{});
+        static_assert(NS <= 4, "short form holds at most four K-steps");
+        __syncthreads();
+        store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0);
+    } else {
+        // ---- pipeline -----------------------------------------------------
+        // NS - 1 stages of loads in flight; the fragments of stage k + 1 are
+        // read from LDS while the MFMAs of stage k run.  The barrier of step
+        // k certifies that stage k + 1 has landed everywhere and that every
+        // wave is done with step k - 1, so buffer (k - 1) mod NS takes stage
+        // k + NS - 1.
+        set_tap();
+#pragma unroll
+        for (int s = 0; s < NS - 1; ++s)
+            issue(s);
+        stage_barrier<LPS *(NS - 2)>();
+        read_frags(0, fa[0], fb[0]);
+        int k = 0;
+        for (; k + 2 <= nk; k += 2) {
+            stage_barrier<LPS *(NS - 3)>();
+            issue(k + NS - 1);
+            read_frags(k + 1, fa[1], fb[1]);
+            mfma(fa[0], fb[0]);
+            stage_barrier<LPS *(NS - 3)>();
+            issue(k + NS);
+            read_frags(k + 2, fa[0], fb[0]);
+            mfma(fa[1], fb[1]);
+        }
+        if (k < nk)
+            mfma(fa[0], fb[0]);
+        wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
+        __syncthreads();
+        store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0);
     }
-    if (k < nk)
-        mfma(fa[0], fb[0]);
-    wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
-    __syncthreads();
-    store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0);
 }
 
 // Padding correction table of the border classes (plan preparation): one
@@ -369,15 +401,21 @@ hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp
     return hipGetLastError();
 }
 
-// DmaTile -> tile, wave grid and stage count.
+// DmaTile -> tile, wave grid, stage count, short-reduction form.
 struct DmaCfg {
     int tc, tp, wc, wp, ns;
+    bool sh;
 };
 static constexpr DmaCfg kDmaCfg[DMA_COUNT] = {
-    {128, 128, 2, 2, 4}, {128, 128, 2, 2, 8}, {128, 64, 2, 2, 4}, {64, 128, 2, 2, 4},
-    {64, 64, 2, 2, 4},   {256, 128, 4, 2, 4}, {128, 256, 2, 4, 4}, {128, 64, 2, 2, 8},
-    {256, 128, 2, 2, 4}, {128, 256, 2, 2, 4}, {128, 128, 1, 2, 8}, {128, 128, 2, 1, 8},
-    {64, 64, 2, 2, 8},   {64, 128, 2, 2, 8},  {64, 64, 2, 2, 16},
+    {128, 128, 2, 2, 4, false}, {128, 128, 2, 2, 8, false}, {128, 64, 2, 2, 4, false},
+    {64, 128, 2, 2, 4, false},  {64, 64, 2, 2, 4, false},   {256, 128, 4, 2, 4, false},
+    {128, 256, 2, 4, 4, false}, {128, 64, 2, 2, 8, false},  {256, 128, 2, 2, 4, false},
+    {128, 256, 2, 2, 4, false}, {128, 128, 1, 2, 8, false}, {128, 128, 2, 1, 8, false},
+    {64, 64, 2, 2, 8, false},   {64, 128, 2, 2, 8, false},  {64, 64, 2, 2, 16, false},
+    {64, 128, 2, 2, 1, true},   {64, 64, 2, 2, 1, true},    {128, 128, 2, 2, 1, true},
+    {128, 64, 2, 2, 1, true},   {64, 128, 2, 2, 2, true},   {128, 128, 2, 2, 2, true},
+    {64, 64, 2, 2, 2, true},    {128, 64, 2, 2, 2, true},   {64, 128, 2, 2, 4, true},
+    {128, 128, 2, 2, 4, true},  {64, 64, 2, 2, 4, true},
 };
 
 TileShape dma_tile_shape(int tile)
@@ -395,16 +433,23 @@ int dma_stages(int tile)
     return kDmaCfg[tile].ns;
 }
 
+bool dma_short(int tile)
+{
+    return kDmaCfg[tile].sh;
+}
+
 template <int T>
 static hipError_t launch_dma_cfg(const ConvArgs &a, hipStream_t st)
 {
     constexpr DmaCfg c = kDmaCfg[T];
     const int grid = (a.ntiles + 7) / 8 * 8;
+    if (c.sh && a.nk > c.ns)
+        return hipErrorInvalidValue;   // more K-steps than the short form holds
     if (a.flip4)
-        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true>), dim3(grid),
+        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, c.sh>), dim3(grid),
                            dim3(c.wc * c.wp * 64), 0, st, a);
     else
-        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false>), dim3(grid),
+        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, c.sh>), dim3(grid),
                            dim3(c.wc * c.wp * 64), 0, st, a);
     return hipGetLastError();
 }

@@ -39,7 +39,7 @@ EXPORTS = [
     "qnn_conv2d", "qnn_depthwise_conv2d", "qnn_dense", "qnn_requantize", "qnn_add",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
     "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_workspace_size",
-    "qnn_plan_describe", "qnn_plan_destroy",
+    "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
 ]
 
 
@@ -115,6 +115,8 @@ def lib() -> ctypes.CDLL:
     L.qnn_plan_workspace_size.restype = ctypes.c_size_t
     L.qnn_plan_describe.argtypes = [P]
     L.qnn_plan_describe.restype = ctypes.c_char_p
+    L.qnn_set_tuning_file.argtypes = [ctypes.c_char_p]
+    L.qnn_set_tuning_file.restype = st
     L.qnn_plan_destroy.argtypes = [P]
     L.qnn_plan_destroy.restype = None
     _lib = L
@@ -204,6 +206,12 @@ def quantize_multiplier(M: float) -> Tuple[int, int]:
     m, s = ctypes.c_int32(), ctypes.c_int32()
     _check(lib().qnn_quantize_multiplier(float(M), ctypes.byref(m), ctypes.byref(s)))
     return m.value, s.value
+
+
+def set_tuning_file(path: Optional[str]):
+    """Read kernel choices from, and append timed ones to, a text file
+    (None: stop); see qnn_set_tuning_file."""
+    _check(lib().qnn_set_tuning_file(None if path is None else os.fsencode(path)))
 
 
 def abi_version() -> int:

@@ -7,7 +7,7 @@ Reads
   * two more of ``bench.py --calibrate-copy MIB`` (a plain copy of known size),
   * the per-layer file bench.py writes (algorithmic bytes per kernel group),
 and writes a markdown summary plus ``traffic.json``, which bench.py reads to
-fill ``roofline.traffic`` as long as the conv kernel source is unchanged.
+fill ``roofline.traffic`` as long as the kernel sources are unchanged.
 
 Usage:
   python -m paper_2006_10226_amd.rocprof_summary --stats D --fetch D --write D \
@@ -24,7 +24,23 @@ import re
 
 _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
 _TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
-_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false)>")
+_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)>")
+_WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
+_STREAM = re.compile(r"conv_stream_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false)>")
+
+
+def kernel_source_sha1(root=None):
+    """SHA-1 over every kernel and library source (csrc/*), in name order:
+    counters taken on other sources no longer describe the kernels."""
+    if root is None:
+        root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    h = hashlib.sha1()
+    d = os.path.join(root, "paper_2006_10226_amd", "csrc")
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(d, name), "rb").read())
+    return h.hexdigest()
 
 
 def group_of(kernel_name):
@@ -40,7 +56,15 @@ def group_of(kernel_name):
     m = _DMA.search(kernel_name)
     if m:
         tc, tp, wc, wp, ns = (int(v) for v in m.groups()[:5])
-        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * 64} stages={ns}"
+        short = "s" if m.group(7) == "true" else ""
+        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * 64} stages={ns}{short}"
+    m = _STREAM.search(kernel_name)
+    if m:
+        tc, tp, wc, wp, nl, ns = (int(v) for v in m.groups()[:6])
+        return f"conv_stream tile={tc}x{tp}x64 threads={(wc * wp + nl) * 64} stages={ns}"
+    m = _WAVE.search(kernel_name)
+    if m:
+        return f"conv_wave tile=64x64x64 threads=256 stages={m.group(2)} split={m.group(1)}"
     base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
     return base
 
@@ -92,8 +116,7 @@ def main():
     args = ap.parse_args()
 
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    src = open(os.path.join(root, "paper_2006_10226_amd", "csrc", "conv_mfma.hip"), "rb").read()
-    sha = hashlib.sha1(src).hexdigest()
+    sha = kernel_source_sha1(root)
 
     stats = read_stats(args.stats)
     layers = json.load(open(args.layers))
@@ -134,7 +157,7 @@ def main():
     for c in args.command:
         lines.append(f"    {c}")
     lines.append("")
-    lines.append(f"conv_mfma.hip sha1 at the time: `{sha}`")
+    lines.append(f"kernel source digest (rocprof_summary.kernel_source_sha1) at the time: `{sha}`")
     lines.append("")
     if args.bench_json:
         lines.append("bench.py line of the unprofiled run:")

@@ -182,3 +182,18 @@ def test_dense_and_depthwise_validation(Q):
     st = L.qnn_depthwise_conv2d(None, FAKE, Q.UINT8, 1, 8, 8, 16, q1.q, FAKE, 3, 3, Q._Q([0.1] * 8, [0] * 8, 8).q,
                                 None, Q.ConvParams(1, 1, 1, 1, 1, 1, 1, 1), FAKE, Q.UINT8, q1.q, none, 0, 16, 0)
     assert Q.STATUS[st] == "QNN_ERR_QPARAM"     # 8 weight scales for 16 channels
+
+
+def test_tuning_file_paths(Q, tmp_path):
+    """The kernel-choice file: a missing file starts empty, a readable one
+    is parsed, an unreadable path is an error, None switches it off."""
+    missing = tmp_path / "none.txt"
+    Q.set_tuning_file(str(missing))
+    assert not missing.exists()          # nothing is written before a plan is timed
+    f = tmp_path / "tune.txt"
+    f.write_text("conv:x0:n1:h8 2 4\nconv:x1:n1:h8 3 1\ngarbage\n")
+    Q.set_tuning_file(str(f))
+    with pytest.raises(Q.QnnError) as e:
+        Q.set_tuning_file(str(f / "below_a_file"))
+    assert e.value.status_name == "QNN_ERR_UNSUPPORTED"
+    Q.set_tuning_file(None)

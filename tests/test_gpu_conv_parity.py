@@ -319,10 +319,27 @@ TAP_SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("tile", list(range(15)))
+# 1x1 convolutions with one to four K-steps (the short-reduction forms of
+# the LDS-direct kernel): ragged pixels and channels, stride 2, padding,
+# int8 input and output, term 3, int32 output
+SHORT_SHAPES = [
+    (W.ConvLayer("s", 9, 9, 64, 300, 1, 1), 5, {}),
+    (W.ConvLayer("s", 9, 11, 128, 72, 1, 1, 2), 3, dict(yt="i8")),
+    (W.ConvLayer("s", 7, 5, 256, 200, 1, 1), 4, dict(zp_w="channel")),
+    (W.ConvLayer("s", 8, 8, 64, 96, 1, 1, 1, (1, 1, 1, 1)), 2, dict(x_dtype="i8")),
+    (W.ConvLayer("s", 6, 6, 192, 64, 1, 1), 3, {}),
+    (W.ConvLayer("s", 10, 10, 128, 130, 1, 1), 2, dict(yt="i32")),
+]
+# K-steps each LDS-direct configuration holds in its short form (0: ring)
+DMA_SHORT_STAGES = [0] * 15 + [1, 1, 1, 1, 2, 2, 2, 2, 4, 4, 4]
+
+
+@pytest.mark.parametrize("tile", list(range(26)))
 def test_every_dma_tile(tile):
+    short = DMA_SHORT_STAGES[tile]
+    shapes = TAP_SHAPES if not short else [sh for sh in SHORT_SHAPES if (sh[0].Cin + 63) // 64 <= short]
     with env(QNN_DMA=tile):
-        for i, (layer, N, kw) in enumerate(TAP_SHAPES):
+        for i, (layer, N, kw) in enumerate(shapes):
             c = W.conv_case(layer, N, seed=100 + tile * 10 + i, **kw)
             p, keep = make_plan(c)
             assert p.describe().startswith("conv_dma"), p.describe()
@@ -330,9 +347,61 @@ def test_every_dma_tile(tile):
             log(f"dma tile {tile} shape {i}")
             assert_equal(run_gpu(c), run_oracle(c), f"dma tile {tile} shape {i} {kw}")
         # zero point 0: no padding correction table
-        c = W.conv_case(TAP_SHAPES[0][0], 2, seed=7)
+        c = W.conv_case(shapes[0][0], 2, seed=7)
         c.zp_x = 0
         assert_equal(run_gpu(c), run_oracle(c), f"dma tile {tile} zp_x 0")
+
+
+@pytest.mark.parametrize("tile", list(range(4)))
+@pytest.mark.parametrize("nx", [None, 1, 3])
+def test_every_stream_tile(tile, nx):
+    """The persistent streaming kernel, forced, on the tap-kernel shapes
+    (ragged tiles, padding, strides, int8 input and output, term 3), with
+    its own grid and with one or three workgroups per XCD so that every
+    workgroup walks many tiles; int32 outputs and half-away rounding are not
+    its cases and plan another kernel."""
+    cfg = dict(QNN_STREAM=tile) if nx is None else dict(QNN_STREAM=tile, QNN_STREAM_NX=nx)
+    with env(**cfg):
+        ran = 0
+        for i, (layer, N, kw) in enumerate(TAP_SHAPES):
+            c = W.conv_case(layer, N, seed=400 + tile * 10 + i, **kw)
+            p, keep = make_plan(c)
+            d = p.describe()
+            p.close()
+            if not d.startswith("conv_stream"):
+                assert kw.get("yt") == "i32" or kw.get("rounding") == "half_away", d
+                continue
+            log(f"stream tile {tile} nx {nx} shape {i}: {d}")
+            assert_equal(run_gpu(c), run_oracle(c), f"stream tile {tile} nx {nx} shape {i} {kw}")
+            ran += 1
+        assert ran >= 5
+        c = W.conv_case(TAP_SHAPES[0][0], 2, seed=9)
+        c.zp_x = 0
+        assert_equal(run_gpu(c), run_oracle(c), f"stream tile {tile} nx {nx} zp_x 0")
+
+
+@pytest.mark.parametrize("coff", [8, 64])
+def test_stream_channel_slice_output(coff):
+    """Streaming kernel writing a channel slice of a wider output (y_ldc,
+    y_coff): 16-byte aligned rows use whole-chunk stores, others byte
+    stores; bytes outside the slice stay untouched."""
+    layer = W.ConvLayer("slice", 12, 13, 64, 72, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 3, seed=31)
+    total = 160
+    with env(QNN_STREAM=0, QNN_STREAM_NX=2):
+        p, keep = make_plan(c, y_ldc=total, y_coff=coff)
+        d = p.describe()
+        assert d.startswith("conv_stream"), d
+        out = torch.full((3, 12, 13, total), 77, dtype=torch.uint8, device="cuda")
+        p.run(dev(c.x), out=out)
+        torch.cuda.synchronize()
+        p.close()
+    y = out.cpu().numpy()
+    log(f"stream slice coff={coff}: {d}")
+    assert_equal(y[..., coff:coff + 72], run_oracle(c), f"stream slice {coff}")
+    rest = np.ones(total, bool)
+    rest[coff:coff + 72] = False
+    assert (y[..., rest] == 77).all()
 
 
 @pytest.mark.parametrize("tile", list(range(12)))
@@ -380,6 +449,31 @@ def test_autotuned_choice_is_a_candidate_and_exact():
     assert_equal(run_gpu(c), run_oracle(c), d)
 
 
+def test_tuning_file_reuses_the_timed_choice(tmp_path):
+    """A timed kernel choice is appended to the kernel-choice file; a plan of
+    the same shape created after re-reading the file takes it without
+    timing and still computes the oracle's bytes."""
+    f = tmp_path / "tune.txt"
+    layer = W.ConvLayer("tuned", 14, 14, 256, 256, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 2, seed=17)
+    Q.set_tuning_file(str(f))
+    try:
+        p, keep = make_plan(c)
+        d1 = p.describe()
+        p.close()
+        lines = f.read_text().split("\n")
+        assert len([ln for ln in lines if ln]) == 1, lines
+        Q.set_tuning_file(str(f))
+        p, keep = make_plan(c)
+        d2 = p.describe()
+        p.close()
+        assert d1.split(" cands=")[0] == d2.split(" cands=")[0], (d1, d2)
+        assert len([ln for ln in f.read_text().split("\n") if ln]) == 1
+        assert_equal(run_gpu(c), run_oracle(c), d2)
+    finally:
+        Q.set_tuning_file(None)
+
+
 @pytest.mark.parametrize("split", [1, 2, 4])
 def test_every_wave_split(split):
     """The wave-independent kernel with 1, 2 and 4 waves sharing a tile's
@@ -408,16 +502,19 @@ def test_every_wave_split(split):
 def test_row_pair_mode(layer, N):
     """Small channel counts (S * C4 <= 32) through the row-pair mode of the
     LDS-direct kernel (zero-point padded image, two filter rows per
-    K-step), for every configuration the plan may pick."""
-    for tile in (None, 0, 3, 4, 12):
-        cfg = {} if tile is None else dict(QNN_DMA=tile)
+    K-step), for every configuration the plan may pick, in the
+    one-tile-per-workgroup kernel and in the streaming one."""
+    cfgs = [{}] + [dict(QNN_DMA=t) for t in (0, 3, 4, 12, 15, 19, 23, 24, 25)]
+    cfgs += [dict(QNN_STREAM=t, QNN_STREAM_NX=nx) for t in range(4) for nx in (2, 64)]
+    for cfg in cfgs:
+        tile = cfg
         for kw in ({}, dict(x_dtype="i8", yt="i8")):
             c = W.conv_case(layer, N, seed=17, **kw)
             with env(**cfg):
                 p, keep = make_plan(c)
             d = p.describe()
             p.close()
-            assert d.startswith("conv_dma"), d
+            assert d.startswith("conv_stream" if "QNN_STREAM" in cfg else ("conv_dma", "conv_stream")), d
             with env(**cfg):
                 got = run_gpu(c)
             assert_equal(got, run_oracle(c), f"{layer.name} tile {tile} {kw}: {d}")
