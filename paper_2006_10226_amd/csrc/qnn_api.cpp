@@ -140,7 +140,7 @@ enum PlanKind { PLAN_CONV = 0, PLAN_DW = 1, PLAN_REQ = 2 };
 }  // namespace
 
 // One implicit-GEMM kernel configuration: family and tile enum value.
-enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3, FAM_STREAM = 4 };
+enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3 };
 struct ConvKernel {
     int fam = FAM_GATHER;
     int tile = TILE_64x64;
@@ -298,7 +298,6 @@ TileShape kernel_shape(const ConvKernel &k)
 {
     switch (k.fam) {
     case FAM_WAVE: return {64, 64, 64};
-    case FAM_STREAM: return stream_tile_shape(k.tile);
     case FAM_DMA: return dma_tile_shape(k.tile);
     case FAM_TAP: return tap_tile_shape(k.tile);
     default: return tile_shape(k.tile);
@@ -307,38 +306,16 @@ TileShape kernel_shape(const ConvKernel &k)
 
 int device_cus();
 
-// Resident workgroups per XCD of a streaming configuration (the grid of the
-// persistent kernel), given its border-class table.
-// 0 when a workgroup does not fit on a CU at all.
-int64_t stream_per_xcd(int tile, size_t ncls, bool pcorr)
-{
-    const size_t dyn = pcorr ? (ncls + 1) * (size_t)stream_tile_shape(tile).tc * sizeof(int32_t) : 0;
-    return (int64_t)device_cus() * stream_blocks_per_cu(tile, dyn) / 8;
-}
-
-// The streaming kernel keeps one channel tile per workgroup: the workgroups
-// of an XCD must cover every channel tile.
-bool stream_fits(int tile, int K, size_t ncls, bool pcorr)
-{
-    const int tc = stream_tile_shape(tile).tc;
-    return (K + tc - 1) / tc <= stream_per_xcd(tile, ncls, pcorr);
-}
-
 // Candidate kernels for a conv of M pixels x K channels with C4 channels
-// per tap and reduction J.  QNN_DMA / QNN_TAP / QNN_TILE / QNN_STREAM=<n>
-// force one configuration when it is eligible (for sweeps and tests).
-// stream_ok: the streaming kernel's conditions other than its tiling
-// (LDS-direct eligible, 8-bit output staged through LDS, 32-bit requantize).
-std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool tap_ok, bool dma_ok, bool stream_ok,
-                                        size_t ncls, bool pcorr)
+// per tap and reduction J.  QNN_DMA / QNN_TAP / QNN_TILE=<n> force one
+// configuration when it is eligible (for sweeps and tests).
+std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool tap_ok, bool dma_ok)
 {
     (void)M;
+    (void)K;
     std::vector<ConvKernel> c;
-    auto stream_fits = [&](int t) { return stream_ok && ::stream_fits(t, K, ncls, pcorr); };
     const int f_dma = env_int("QNN_DMA", -1), f_tap = env_int("QNN_TAP", -1), f_tile = env_int("QNN_TILE", -1);
-    const int f_wave = env_int("QNN_WAVE", -1), f_stream = env_int("QNN_STREAM", -1);
-    if (f_stream >= 0 && f_stream < STREAM_COUNT && stream_fits(f_stream))
-        return {{FAM_STREAM, f_stream}};
+    const int f_wave = env_int("QNN_WAVE", -1);
     if ((f_wave == 1 || f_wave == 2 || f_wave == 4) && dma_ok)
         return {{FAM_WAVE, f_wave}};
     if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok && (!dma_short(f_dma) || (J + 63) / 64 <= dma_stages(f_dma)))
@@ -347,10 +324,6 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
         return {{FAM_TAP, f_tap}};
     if (f_tile >= 0 && f_tile < TILE_COUNT)
         return {{FAM_GATHER, f_tile}};
-    if (env_int("QNN_STREAM", -1) != -2)
-        for (int t = 0; t < STREAM_COUNT; ++t)
-            if (stream_fits(t))
-                c.push_back({FAM_STREAM, t});
     if (dma_ok && env_int("QNN_WAVE", -1) != -2)
         for (int sp : {1, 2, 4})
             if (sp == 1 || J / 64 >= 2 * sp)
@@ -380,7 +353,7 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
 void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr_tab, const uint8_t *pcls_tab)
 {
     const TileShape ts = kernel_shape(k);
-    const bool zero_pad = k.fam == FAM_DMA || k.fam == FAM_WAVE || k.fam == FAM_STREAM;   // x = 0 outside the image
+    const bool zero_pad = k.fam == FAM_DMA || k.fam == FAM_WAVE;   // gathers read x = 0 outside the image
     a.pcorr = zero_pad ? pcorr_tab : nullptr;
     a.pcls = zero_pad ? pcls_tab : nullptr;
     const int64_t tiles_c = (a.K + ts.tc - 1) / ts.tc;
@@ -396,26 +369,12 @@ void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr
         const int64_t resident = (int64_t)device_cus() * conv_blocks_per_cu(k.tile, avec, dyn);
         a.nblocks = (int)std::min<int64_t>((ntiles + 7) / 8 * 8, std::max<int64_t>(8, resident / 8 * 8));
     }
-    if (k.fam == FAM_STREAM && a.ntiles >= 0) {
-        // XCD x owns the x-th eighth of the tiles; its nx workgroups (a
-        // multiple of the channel tile count, so that each keeps one channel
-        // tile) take them in turn.  QNN_STREAM_NX caps nx (tests use it to
-        // give every workgroup many tiles).
-        a.chunk = (int)((ntiles + 7) / 8);
-        int64_t nx = std::min<int64_t>(stream_per_xcd(k.tile, (size_t)a.ncls, a.pcorr != nullptr), a.chunk);
-        const int cap = env_int("QNN_STREAM_NX", 0);
-        if (cap > 0)
-            nx = std::min<int64_t>(nx, cap);
-        nx = std::max<int64_t>(tiles_c, nx / tiles_c * tiles_c);
-        a.nblocks = (int)(8 * nx);
-    }
 }
 
 hipError_t launch_conv_kernel(const ConvArgs &a, const ConvKernel &k, int avec, hipStream_t st)
 {
     switch (k.fam) {
     case FAM_WAVE: return launch_conv_wave(a, k.tile, st);
-    case FAM_STREAM: return launch_conv_stream(a, k.tile, st);
     case FAM_DMA: return launch_conv_dma(a, k.tile, st);
     case FAM_TAP: return launch_conv_tap(a, k.tile, st);
     default: return launch_conv(a, k.tile, avec, st);
@@ -747,19 +706,12 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         if (shift[k] < 33 || shift[k] > 53)
             fast = false;
     const bool staged = d.yt != QNN_INT32 && env_int("QNN_STAGED", 1) != 0;
-    const bool stream_ok = dma_ok && fast && staged;
     std::vector<ConvKernel> cands;
     if (rowpack) {
-        const int f = env_int("QNN_DMA", -1), fs = env_int("QNN_STREAM", -1);
-        if (fs >= 0 && fs < STREAM_COUNT && fast && staged && stream_fits(fs, d.K, 0, false)) {
-            cands.push_back({FAM_STREAM, fs});
-        } else if (f >= 0 && f < DMA_COUNT && (!dma_short(f) || npairs <= dma_stages(f))) {
+        const int f = env_int("QNN_DMA", -1);
+        if (f >= 0 && f < DMA_COUNT && (!dma_short(f) || npairs <= dma_stages(f))) {
             cands.push_back({FAM_DMA, f});
         } else {
-            if (fast && staged && fs != -2)
-                for (int t = 0; t < STREAM_COUNT; ++t)
-                    if (stream_fits(t, d.K, 0, false))
-                        cands.push_back({FAM_STREAM, t});
             for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_128x64_S8, DMA_64x128_S8,
                           DMA_64x64_S8})
                 cands.push_back({FAM_DMA, t});
@@ -768,7 +720,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
                     cands.push_back({FAM_DMA, t});
         }
     } else {
-        cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok, stream_ok, ncls, pcorr);
+        cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok);
     }
 
     const size_t wp_bytes = align_up((size_t)Kpad * Jpad, 256);
@@ -862,7 +814,6 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     a.hi_off = hi + off8;
     a.out_xor = off8 ? 0x80808080u : 0u;
     a.staged = staged;
-    a.ncls = (int)ncls;
     a.zp4 = 0x01010101u * (uint32_t)(uint8_t)zpx_l;
     const int32_t *pcorr_tab = pcorr ? corr_d : nullptr;
     const uint8_t *pcls_tab = pcorr ? pcls_d : nullptr;
@@ -909,7 +860,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
     }
     const TileShape ts = kernel_shape(best);
-    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave", "conv_stream"};
+    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave"};
     char buf[200];
     if (best.fam == FAM_GATHER)
         snprintf(buf, sizeof buf,
@@ -920,14 +871,8 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         snprintf(buf, sizeof buf,
                  "%s tile=%dx%dx%d threads=%d stages=%d%s tiles=%d term3=%d border=%d M=%lld K=%d J=%lld cands=%d",
                  fam_name[best.fam], ts.tc, ts.tp, ts.bk,
-                 best.fam == FAM_DMA      ? dma_threads(best.tile)
-                 : best.fam == FAM_WAVE   ? 256
-                 : best.fam == FAM_STREAM ? stream_threads(best.tile)
-                                          : tap_threads(best.tile),
-                 best.fam == FAM_DMA      ? dma_stages(best.tile)
-                 : best.fam == FAM_WAVE   ? 4
-                 : best.fam == FAM_STREAM ? stream_stages(best.tile)
-                                          : 2,
+                 best.fam == FAM_DMA ? dma_threads(best.tile) : best.fam == FAM_WAVE ? 256 : tap_threads(best.tile),
+                 best.fam == FAM_DMA ? dma_stages(best.tile) : best.fam == FAM_WAVE ? 4 : 2,
                  best.fam == FAM_DMA && dma_short(best.tile) ? "s" : "", a.ntiles, (int)term3,
                  (int)ncls, (long long)M, d.K, (long long)Jg, (int)cands.size());
     if (best.fam == FAM_WAVE) {
@@ -1371,7 +1316,7 @@ qnn_status qnn_set_tuning_file(const char *path)
             char key[256];
             int fam = 0, tile = 0;
             while (std::fscanf(f, "%255s %d %d", key, &fam, &tile) == 3)
-                if (fam >= FAM_GATHER && fam <= FAM_STREAM && tile >= 0)
+                if (fam >= FAM_GATHER && fam <= FAM_WAVE && tile >= 0)
                     rec[key] = ConvKernel{fam, tile};
             std::fclose(f);
         }

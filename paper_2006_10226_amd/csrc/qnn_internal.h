@@ -62,9 +62,6 @@ struct ConvArgs {
     // padded image (H, W padded, pads 0), R counts filter row pairs, S is 1,
     // and row_bytes is the padded image's row stride
     int32_t rowpack, row_bytes;
-    // streaming kernel (conv_stream.hip): tiles per XCD share and number of
-    // border classes in pcorr
-    int32_t chunk, ncls;
 };
 
 // Depthwise conv arguments (channel multiplier 1).
@@ -190,24 +187,6 @@ hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp
                             uint8_t zp, uint8_t *out, hipStream_t st);
 hipError_t launch_border_corr(const int8_t *wp, int Kpad, int Jpad, int C4, int S, int RS, const uint32_t *rmask,
                               const uint32_t *cmask, int ncls, int32_t zpx, int32_t *corr, hipStream_t st);
-// Tile configurations of the persistent streaming kernel (conv_stream.hip):
-// channels x pixels, compute waves + loader waves, LDS stages; K-step 64,
-// C % 64 == 0, requantized 8-bit output.
-enum StreamTile {
-    STREAM_64x128 = 0,    // 2x2 compute waves of 32x64, 2 loader waves, 5 stages
-    STREAM_64x64 = 1,     // 2x2 compute waves of 32x32, 1 loader wave, 8 stages
-    STREAM_128x64 = 2,    // 2x2 compute waves of 64x32, 1 loader wave, 5 stages
-    STREAM_128x128 = 3,   // 2x2 compute waves of 64x64, 2 loader waves, 4 stages
-    STREAM_COUNT
-};
-TileShape stream_tile_shape(int tile);
-int stream_threads(int tile);
-int stream_stages(int tile);
-// Resident workgroups per CU of a streaming configuration with dyn_lds
-// bytes of dynamic LDS (the border-class correction table); 0 when it does
-// not fit.
-int stream_blocks_per_cu(int tile, size_t dyn_lds);
-hipError_t launch_conv_stream(const ConvArgs &a, int tile, hipStream_t st);
 int tap_threads(int tile);
 hipError_t launch_conv_tap(const ConvArgs &a, int tile, hipStream_t st);
 

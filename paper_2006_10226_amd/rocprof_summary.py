@@ -26,7 +26,6 @@ _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\
 _TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
 _DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)>")
 _WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
-_STREAM = re.compile(r"conv_stream_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false)>")
 
 
 def kernel_source_sha1(root=None):
@@ -58,10 +57,6 @@ def group_of(kernel_name):
         tc, tp, wc, wp, ns = (int(v) for v in m.groups()[:5])
         short = "s" if m.group(7) == "true" else ""
         return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * 64} stages={ns}{short}"
-    m = _STREAM.search(kernel_name)
-    if m:
-        tc, tp, wc, wp, nl, ns = (int(v) for v in m.groups()[:6])
-        return f"conv_stream tile={tc}x{tp}x64 threads={(wc * wp + nl) * 64} stages={ns}"
     m = _WAVE.search(kernel_name)
     if m:
         return f"conv_wave tile=64x64x64 threads=256 stages={m.group(2)} split={m.group(1)}"

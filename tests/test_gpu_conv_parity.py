@@ -352,53 +352,29 @@ def test_every_dma_tile(tile):
         assert_equal(run_gpu(c), run_oracle(c), f"dma tile {tile} zp_x 0")
 
 
-@pytest.mark.parametrize("tile", list(range(4)))
-@pytest.mark.parametrize("nx", [None, 1, 3])
-def test_every_stream_tile(tile, nx):
-    """The persistent streaming kernel, forced, on the tap-kernel shapes
-    (ragged tiles, padding, strides, int8 input and output, term 3), with
-    its own grid and with one or three workgroups per XCD so that every
-    workgroup walks many tiles; int32 outputs and half-away rounding are not
-    its cases and plan another kernel."""
-    cfg = dict(QNN_STREAM=tile) if nx is None else dict(QNN_STREAM=tile, QNN_STREAM_NX=nx)
-    with env(**cfg):
-        ran = 0
-        for i, (layer, N, kw) in enumerate(TAP_SHAPES):
-            c = W.conv_case(layer, N, seed=400 + tile * 10 + i, **kw)
-            p, keep = make_plan(c)
-            d = p.describe()
-            p.close()
-            if not d.startswith("conv_stream"):
-                assert kw.get("yt") == "i32" or kw.get("rounding") == "half_away", d
-                continue
-            log(f"stream tile {tile} nx {nx} shape {i}: {d}")
-            assert_equal(run_gpu(c), run_oracle(c), f"stream tile {tile} nx {nx} shape {i} {kw}")
-            ran += 1
-        assert ran >= 5
-        c = W.conv_case(TAP_SHAPES[0][0], 2, seed=9)
-        c.zp_x = 0
-        assert_equal(run_gpu(c), run_oracle(c), f"stream tile {tile} nx {nx} zp_x 0")
-
-
+@pytest.mark.parametrize("layer,tile", [
+    (W.ConvLayer("slice3x3", 12, 13, 64, 72, 3, 3, 1, (1, 1, 1, 1)), 3),
+    (W.ConvLayer("slice1x1", 12, 13, 64, 72, 1, 1), 15),
+    (W.ConvLayer("slice1x1", 12, 13, 192, 72, 1, 1), 23),
+], ids=["ring", "short1", "short4"])
 @pytest.mark.parametrize("coff", [8, 64])
-def test_stream_channel_slice_output(coff):
-    """Streaming kernel writing a channel slice of a wider output (y_ldc,
-    y_coff): 16-byte aligned rows use whole-chunk stores, others byte
-    stores; bytes outside the slice stay untouched."""
-    layer = W.ConvLayer("slice", 12, 13, 64, 72, 3, 3, 1, (1, 1, 1, 1))
+def test_dma_channel_slice_output(layer, tile, coff):
+    """LDS-direct kernel writing a channel slice of a wider output (y_ldc,
+    y_coff): 16-byte aligned rows take the staged whole-chunk stores, others
+    the direct ones; bytes outside the slice stay untouched."""
     c = W.conv_case(layer, 3, seed=31)
     total = 160
-    with env(QNN_STREAM=0, QNN_STREAM_NX=2):
+    with env(QNN_DMA=tile):
         p, keep = make_plan(c, y_ldc=total, y_coff=coff)
         d = p.describe()
-        assert d.startswith("conv_stream"), d
+        assert d.startswith("conv_dma"), d
         out = torch.full((3, 12, 13, total), 77, dtype=torch.uint8, device="cuda")
         p.run(dev(c.x), out=out)
         torch.cuda.synchronize()
         p.close()
     y = out.cpu().numpy()
-    log(f"stream slice coff={coff}: {d}")
-    assert_equal(y[..., coff:coff + 72], run_oracle(c), f"stream slice {coff}")
+    log(f"dma slice coff={coff}: {d}")
+    assert_equal(y[..., coff:coff + 72], run_oracle(c), f"dma slice {coff}")
     rest = np.ones(total, bool)
     rest[coff:coff + 72] = False
     assert (y[..., rest] == 77).all()
@@ -502,19 +478,16 @@ def test_every_wave_split(split):
 def test_row_pair_mode(layer, N):
     """Small channel counts (S * C4 <= 32) through the row-pair mode of the
     LDS-direct kernel (zero-point padded image, two filter rows per
-    K-step), for every configuration the plan may pick, in the
-    one-tile-per-workgroup kernel and in the streaming one."""
+    K-step), for every configuration the plan may pick."""
     cfgs = [{}] + [dict(QNN_DMA=t) for t in (0, 3, 4, 12, 15, 19, 23, 24, 25)]
-    cfgs += [dict(QNN_STREAM=t, QNN_STREAM_NX=nx) for t in range(4) for nx in (2, 64)]
     for cfg in cfgs:
-        tile = cfg
         for kw in ({}, dict(x_dtype="i8", yt="i8")):
             c = W.conv_case(layer, N, seed=17, **kw)
             with env(**cfg):
                 p, keep = make_plan(c)
             d = p.describe()
             p.close()
-            assert d.startswith("conv_stream" if "QNN_STREAM" in cfg else ("conv_dma", "conv_stream")), d
+            assert d.startswith("conv_dma"), d
             with env(**cfg):
                 got = run_gpu(c)
-            assert_equal(got, run_oracle(c), f"{layer.name} tile {tile} {kw}: {d}")
+            assert_equal(got, run_oracle(c), f"{layer.name} {cfg} {kw}: {d}")
