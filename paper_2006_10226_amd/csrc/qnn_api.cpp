@@ -328,6 +328,10 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
         for (int sp : {1, 2, 4})
             if (sp == 1 || J / 64 >= 2 * sp)
                 c.push_back({FAM_WAVE, sp});
+    if (tap_ok && env_int("QNN_TAP", -1) != -2)
+        for (int t = 0; t < TAP_COUNT; ++t)
+            if (C4 % tap_tile_shape(t).bk == 0)
+                c.push_back({FAM_TAP, t});
     if (dma_ok && env_int("QNN_DMA", -1) != -2) {
         for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_256x128_S4, DMA_128x256_S4,
                       DMA_128x128_S8, DMA_128x64_S8, DMA_64x64_S8, DMA_64x128_S8, DMA_64x64_S16})
