@@ -304,6 +304,13 @@ def main():
     log(f"{len(items)} layers, {total_macs / 1e9:.2f} G MAC per step")
 
     ms, graphed = time_steps(items, args.steps, args.warmup, not args.no_graph)
+    if graphed:
+        # a graph replay has a fixed launch cost that dominates a step of
+        # one or two small layers; such steps are timed as eager launches
+        ms_eager, _ = time_steps(items, args.steps, args.warmup, False)
+        log(f"step {ms:.4f} ms from a graph, {ms_eager:.4f} ms eager")
+        if ms_eager < ms:
+            ms, graphed = ms_eager, False
     value = 2.0 * total_macs / (ms * 1e-3) / 1e12
     log(f"step {ms:.4f} ms -> {value:.1f} TOP/s (graph={graphed})")
 
@@ -339,6 +346,8 @@ def main():
     roof["avg_launch_us_event_bracketed"] = round(D["ms"] / D["launches"] * 1e3, 3)
     roof["launches_per_step"] = D["launches"]
 
+    roof_us = sum(max(2.0 * it.macs / (PEAK_INT8_TOPS * 1e12), it.bytes / (PEAK_HBM_GBS * 1e9)) * 1e6
+                  for it in items)
     layer_rows = []
     for it, t in zip(items, per):
         row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3),
@@ -346,6 +355,7 @@ def main():
         if it.macs:
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
         row["gbs"] = round(it.bytes / (float(t) * 1e-3) / 1e9, 1)
+        row["roofline_us"] = round(max(2.0 * it.macs / (PEAK_INT8_TOPS * 1e12), it.bytes / (PEAK_HBM_GBS * 1e9)) * 1e6, 3)
         layer_rows.append(row)
     if args.layers_out:
         os.makedirs(os.path.dirname(os.path.abspath(args.layers_out)), exist_ok=True)
@@ -376,7 +386,10 @@ def main():
         "data": "synthetic (seeded, architecture shapes only, random weights)",
         "config": {"workload": args.workload, "batch": batch, "layers": len(items),
                    "gmac_per_step": round(total_macs / 1e9, 3), "launch": "hipGraph" if graphed else "eager",
-                   "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4)},
+                   "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4),
+                   # sum over layers of max(MFMA time at peak, algorithmic bytes at HBM peak),
+                   # over the measured step: the whole stack's fraction of its roofline
+                   "stack_roofline_frac": round(roof_us / (ms * 1e3), 4)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }
