@@ -160,6 +160,8 @@ struct qnn_plan {
     uint8_t pad_zp = 0;         // zero point byte written into padded channels
     // depthwise
     DwArgs dw{};
+    bool dw3 = false;               // the 3x3 dot-product kernel applies
+    const ChanRec *chan3 = nullptr; // its channel records (constant with the zero-point terms)
     // requantize
     ReqArgs req{};
     int xdt = 0, ydt = 0;
@@ -617,26 +619,61 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     if (d.depthwise) {
         p->kind = PLAN_DW;
         const int C = d.C, RS = d.R * d.S;
+        // 3x3 layers run on the dot-product kernel; the general kernel's
+        // weights are kept too (unaligned x, other filter sizes)
+        const int64_t dw3_items = (int64_t)d.N * Ho * ((Wo + dw3_pixels() - 1) / dw3_pixels()) * (C / 8);
+        const bool dw3 = d.R == 3 && d.S == 3 && d.cp.dil_h == 1 && d.cp.dil_w == 1 && C % 8 == 0 &&
+                         (d.cp.stride_w == 1 || d.cp.stride_w == 2) && dw3_items < (int64_t(1) << 31) &&
+                         (int64_t)d.N * d.H * d.W * C < (int64_t(1) << 31) &&
+                         (int64_t)M * d.y_ldc * (d.yt == QNN_INT32 ? 4 : 1) < (int64_t(1) << 31) &&
+                         env_int("QNN_DW3", 1) != 0;
+        const int32_t zpx_l = d.xt == QNN_UINT8 ? zpx - 128 : zpx;
+        const int32_t zpy = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
+        const int32_t off8 = d.yt == QNN_INT8 ? 128 : 0;
+        bool fast = d.yt != QNN_INT32 && d.rnd == QNN_ROUND_HALF_UP;
+        for (int c = 0; c < C; ++c)
+            if (shift[c] < 33 || shift[c] > 53)
+                fast = false;
+        bool zpw_any = false;
+        for (int i = 0; i < d.wq.n; ++i)
+            zpw_any = zpw_any || d.wq.zero_point[i] != 0;
         const size_t wq_bytes = align_up(sizeof(int32_t) * RS * C, 256);
         const size_t ch_bytes = align_up(sizeof(ChanRec) * C, 256);
         const size_t zw_bytes = align_up(sizeof(int32_t) * C, 256);
-        hipError_t e = hipMalloc(&p->dev, wq_bytes + ch_bytes + zw_bytes);
+        const size_t wd_bytes = dw3 ? align_up(sizeof(uint32_t) * 3 * C, 256) : 0;
+        const size_t ch3_bytes = dw3 ? ch_bytes : 0;
+        const size_t total = wq_bytes + ch_bytes + zw_bytes + wd_bytes + ch3_bytes;
+        hipError_t e = hipMalloc(&p->dev, total);
         if (e != hipSuccess) {
             free_plan(p);
-            return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", wq_bytes + ch_bytes + zw_bytes);
+            return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes failed", total);
         }
         int32_t *wq = (int32_t *)p->dev;
         ChanRec *chan = (ChanRec *)((char *)p->dev + wq_bytes);
         int32_t *zpw_d = (int32_t *)((char *)p->dev + wq_bytes + ch_bytes);
+        uint32_t *wd = dw3 ? (uint32_t *)((char *)zpw_d + zw_bytes) : nullptr;
+        ChanRec *chan3 = dw3 ? (ChanRec *)((char *)zpw_d + zw_bytes + wd_bytes) : nullptr;
         std::vector<uint8_t> host(ch_bytes + zw_bytes, 0);
+        std::vector<ChanRec> host3(dw3 ? C : 0);
         for (int c = 0; c < C; ++c) {
             const ChanRec r{mult[c], 0, 0, shift[c]};
             const int32_t z = d.wq.zero_point[d.wq.n == 1 ? 0 : c];
             std::memcpy(host.data() + sizeof(ChanRec) * c, &r, sizeof r);
             std::memcpy(host.data() + ch_bytes + sizeof(int32_t) * c, &z, sizeof z);
+            if (dw3) {
+                ChanRec r3{mult[c], 0, 0, shift[c]};
+                if (fast) {
+                    const int sh = shift[c] - 32;
+                    r3.rndzp = (int32_t)((1LL << (sh - 1)) + (int64_t)(zpy + off8) * (1LL << sh));
+                }
+                host3[c] = r3;
+            }
         }
         if ((e = hipMemcpyAsync(chan, host.data(), host.size(), hipMemcpyHostToDevice, st)) != hipSuccess ||
+            (dw3 && (e = hipMemcpyAsync(chan3, host3.data(), sizeof(ChanRec) * C, hipMemcpyHostToDevice, st)) !=
+                        hipSuccess) ||
             (e = launch_prep_dw(d.w, d.bias, RS, C, zpw_d, wq, chan, st)) != hipSuccess ||
+            (dw3 && (e = launch_prep_dw3(d.w, d.bias, C, zpx_l, zpw_d, wd, chan3, st)) != hipSuccess) ||
             (e = hipStreamSynchronize(st)) != hipSuccess) {
             free_plan(p);
             return hip_fail(e, "depthwise plan preparation");
@@ -650,12 +687,25 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         a.zp_x = zpx;
         a.x_signed = d.xt == QNN_INT8;
         a.ydt = d.yt; a.lo = lo; a.hi = hi;
-        a.zp_y = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
+        a.zp_y = zpy;
         a.rounding = d.rnd;
         a.y_ldc = d.y_ldc; a.y_coff = d.y_coff;
         a.out_i32 = d.yt == QNN_INT32;
+        a.wd = wd;
+        a.zpw = zpw_d;
+        a.flip4 = d.xt == QNN_UINT8 ? 0x80808080u : 0u;
+        a.zp4 = 0x01010101u * (uint32_t)(uint8_t)zpx_l;
+        a.zpw_any = zpw_any;
+        a.fast_rq = fast;
+        a.lo_off = lo + off8;
+        a.hi_off = hi + off8;
+        a.out_xor = off8 ? 0x80808080u : 0u;
+        a.items = dw3 ? (int32_t)dw3_items : 0;
+        p->dw3 = dw3;
+        p->chan3 = chan3;
         char buf[128];
-        snprintf(buf, sizeof buf, "depthwise %dx%d stride %dx%d M=%lld C=%d", d.R, d.S, a.sh, a.sw, (long long)M, C);
+        snprintf(buf, sizeof buf, "depthwise%s %dx%d stride %dx%d M=%lld C=%d", dw3 ? " dot4" : "", d.R, d.S, a.sh,
+                 a.sw, (long long)M, C);
         p->desc = buf;
         *out = p;
         return QNN_OK;
@@ -946,7 +996,14 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
             return fail(QNN_ERR_NULL, "plan_run: x or y is NULL");
         a.x = (const uint8_t *)x;
         a.y = y;
-        hipError_t e = launch_depthwise(a, st);
+        hipError_t e;
+        if (p->dw3 && ((uintptr_t)x & 7) == 0) {
+            a.chan = p->chan3;
+            a.vec_store = ((uintptr_t)y & 7) == 0 && a.y_ldc % 8 == 0 && a.y_coff % 8 == 0;
+            e = launch_depthwise3(a, st);
+        } else {
+            e = launch_depthwise(a, st);
+        }
         return e == hipSuccess ? QNN_OK : hip_fail(e, "depthwise launch");
     }
     case PLAN_REQ: {

@@ -67,8 +67,8 @@ struct ConvArgs {
 // Depthwise conv arguments (channel multiplier 1).
 struct DwArgs {
     const uint8_t *x;
-    const int32_t *wq;      // [R*S][C] weights minus zero point, int32
-    const ChanRec *chan;    // [C]: mult, bconst (= bias), -, shift
+    const int32_t *wq;      // [R*S][C] weights minus zero point, int32 (general kernel)
+    const ChanRec *chan;    // [C]: mult, bconst, rndzp, shift (bconst: see the kernels)
     void *y;
     int32_t N, H, W, C, Ho, Wo, R, S;
     int32_t sh, sw, pt, pl, dh, dw;
@@ -77,6 +77,17 @@ struct DwArgs {
     int32_t ydt, lo, hi, zp_y, rounding;
     int32_t y_ldc, y_coff;
     int32_t out_i32;        // 1: raw accumulator output
+    // 3x3 dot-product kernel (depthwise.hip)
+    const uint32_t *wd;     // [C][3] words (w[r][0][c], w[r][1][c], w[r][2][c], 0)
+    const int32_t *zpw;     // [C] weight zero points
+    uint32_t flip4;         // 0x80808080 when x is uint8 (legalised to int8), else 0
+    uint32_t zp4;           // legalised zp_x in all four bytes (the padding value)
+    int32_t zpw_any;        // some weight zero point is not 0 (window sums needed)
+    int32_t fast_rq;        // 32-bit requantize (HALF_UP, every shift in [33, 53])
+    int32_t lo_off, hi_off; // clamp + off for the 32-bit path
+    uint32_t out_xor;       // 0x80808080 for int8 outputs of the 32-bit path
+    int32_t vec_store;      // 8-byte output stores allowed
+    int32_t items;          // work items: N * Ho * ceil(Wo / dw3_pixels()) * C / 8 (< 2^31)
 };
 
 // Elementwise requantize / add arguments.
@@ -206,6 +217,11 @@ hipError_t launch_prep_conv(const int8_t *w, const int32_t *bias, int K, int RS,
 hipError_t launch_prep_dw(const int8_t *w, const int32_t *bias, int RS, int C, const int32_t *zpw, int32_t *wq,
                           ChanRec *chan, hipStream_t st);
 hipError_t launch_depthwise(const DwArgs &a, hipStream_t st);
+// 3x3, undilated, C % 8 == 0, stride_w 1 or 2, x 8-byte aligned
+hipError_t launch_prep_dw3(const int8_t *w, const int32_t *bias, int C, int32_t zpx_l, const int32_t *zpw,
+                           uint32_t *wd, ChanRec *chan, hipStream_t st);
+hipError_t launch_depthwise3(const DwArgs &a, hipStream_t st);
+int dw3_pixels();   // output pixels along a row per work item of launch_depthwise3
 hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, hipStream_t st);
 hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned, hipStream_t st);
 

@@ -380,6 +380,68 @@ def test_dma_channel_slice_output(layer, tile, coff):
     assert (y[..., rest] == 77).all()
 
 
+# 3x3 depthwise layers of the dot-product kernel: strides 1 and 2,
+# asymmetric pads, row tails (Wo not a multiple of 4), int8 input and
+# output, int32 output, weight zero points, half-away rounding (64-bit
+# requantize), 8 to 144 channels
+DW3_SHAPES = [
+    (W.ConvLayer("d", 13, 11, 144, 144, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, {}),
+    (W.ConvLayer("d", 14, 15, 96, 96, 3, 3, 2, (0, 0, 1, 1), depthwise=True), 3, dict(x_dtype="i8")),
+    (W.ConvLayer("d", 9, 10, 8, 8, 3, 3, 1, (2, 1, 0, 1), depthwise=True), 2, dict(yt="i8")),
+    (W.ConvLayer("d", 12, 12, 32, 32, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, dict(zp_w="channel")),
+    (W.ConvLayer("d", 11, 9, 16, 16, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2, dict(yt="i32", zp_w="tensor")),
+    (W.ConvLayer("d", 8, 7, 64, 64, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, dict(rounding="half_away")),
+    (W.ConvLayer("d", 5, 5, 24, 24, 3, 3, 1, (0, 0, 0, 0), depthwise=True), 4, dict(act=None)),
+]
+
+
+@pytest.mark.parametrize("i", range(len(DW3_SHAPES)))
+def test_depthwise3x3_dot4(i):
+    """The 3x3 depthwise dot-product kernel against the oracle, and the
+    general depthwise kernel (QNN_DW3=0) on the same case."""
+    layer, N, kw = DW3_SHAPES[i]
+    c = W.conv_case(layer, N, seed=600 + i, **kw)
+    p, keep = make_plan(c)
+    d = p.describe()
+    p.close()
+    assert d.startswith("depthwise dot4"), d
+    log(f"dw3 shape {i}: {d}")
+    ref = run_oracle(c)
+    assert_equal(run_gpu(c), ref, f"dw3 shape {i} {kw}")
+    with env(QNN_DW3=0):
+        assert_equal(run_gpu(c), ref, f"dw general shape {i} {kw}")
+
+
+def test_depthwise3x3_slices_and_unaligned_input():
+    """Channel slices of a wider output (8-byte aligned rows take 8-byte
+    stores, others byte stores) and an input view that is not 8-byte
+    aligned (the general kernel takes over)."""
+    layer = W.ConvLayer("dslice", 10, 9, 48, 48, 3, 3, 1, (1, 1, 1, 1), depthwise=True)
+    c = W.conv_case(layer, 2, seed=77)
+    ref = run_oracle(c)
+    for coff in (0, 5, 16):
+        total = 80
+        p, keep = make_plan(c, y_ldc=total, y_coff=coff)
+        out = torch.full((2, 10, 9, total), 77, dtype=torch.uint8, device="cuda")
+        p.run(dev(c.x), out=out)
+        torch.cuda.synchronize()
+        p.close()
+        y = out.cpu().numpy()
+        assert_equal(y[..., coff:coff + 48], ref, f"dw3 slice {coff}")
+        rest = np.ones(total, bool)
+        rest[coff:coff + 48] = False
+        assert (y[..., rest] == 77).all()
+    # x at an odd byte offset inside a larger buffer
+    buf = torch.zeros(c.x.size + 3, dtype=torch.uint8, device="cuda")
+    xv = buf[3:].view(c.x.shape)
+    xv.copy_(dev(c.x))
+    p, keep = make_plan(c)
+    y = p.run(xv)
+    torch.cuda.synchronize()
+    p.close()
+    assert_equal(y.cpu().numpy(), ref, "dw3 unaligned x")
+
+
 @pytest.mark.parametrize("tile", list(range(12)))
 def test_every_tap_tile(tile):
     with env(QNN_TAP=tile):
