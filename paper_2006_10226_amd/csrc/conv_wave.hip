@@ -20,10 +20,13 @@
 //     the border-class correction as in conv_dma.hip.
 // Waves never wait for each other while accumulating, so the latency of
 // one wave's loads is covered by the other waves on its SIMD and by its own
-// prefetch (activations three stages ahead, weights one).  A workgroup of four waves covers 4 / KSPLIT
-// tiles; with KSPLIT > 1 the waves of a tile take interleaved parts of the
+// prefetch (activations and weights three stages ahead).  A workgroup of
+// four waves covers 4 / KSPLIT tiles (eight waves, one tile, for KSPLIT =
+// 8); with KSPLIT > 1 the waves of a tile take interleaved parts of the
 // reduction and add their partial sums through LDS before the epilogue.
 #include "conv_common.h"
+
+#include <type_traits>
 
 namespace qnn {
 
@@ -54,20 +57,28 @@ __device__ __forceinline__ int sw64w(int row)
 
 }  // namespace
 
+// Waves of a workgroup: four, or KSPLIT when a tile is split eight ways.
+template <int KSPLIT>
+constexpr int wave_count()
+{
+    return KSPLIT > 4 ? KSPLIT : 4;
+}
+
 template <int KSPLIT, int NS, bool FLIP>
-__global__ void __launch_bounds__(256, 2) conv_wave_kernel(ConvArgs a)
+__global__ void __launch_bounds__(wave_count<KSPLIT>() * 64, (KSPLIT > 4 ? 1 : 2)) conv_wave_kernel(ConvArgs a)
 {
     constexpr int BK = 64;
-    constexpr int TPW = 4 / KSPLIT;          // tiles per workgroup
+    constexpr int NWV = wave_count<KSPLIT>();
+    constexpr int TPW = NWV / KSPLIT;        // tiles per workgroup
     constexpr int BSTAGE = 64 * BK;          // activation bytes per stage and wave
     constexpr int RING = NS * BSTAGE;        // LDS ring of one wave
     constexpr int LPS = 8;                   // loads per lane per stage (4 weight, 4 activation)
     static_assert(NS == 4, "stage n + 3 reuses buffer (n - 1) mod 4");
-    static_assert(KSPLIT == 1 || KSPLIT == 2 || KSPLIT == 4, "split");
+    static_assert(KSPLIT == 1 || KSPLIT == 2 || KSPLIT == 4 || KSPLIT == 8, "split");
     // LDS: four wave rings; reused for the partial sums (4 x 16 KB) and the
     // output staging (TPW tiles of 64 pixels x 80 bytes)
-    __shared__ __attribute__((aligned(1024))) int8_t lds[4 * RING];
-    static_assert(4 * RING >= 4 * 64 * 64 * 4, "partial sums must fit");
+    __shared__ __attribute__((aligned(1024))) int8_t lds[NWV * RING];
+    static_assert(RING >= 64 * 64 * 4, "partial sums must fit");
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -206,40 +217,42 @@ __global__ void __launch_bounds__(256, 2) conv_wave_kernel(ConvArgs a)
     };
 
     // ---- main loop ---------------------------------------------------------
-    // activations run three stages ahead through the LDS ring, weights one
-    // stage ahead through two register sets.  Step n first issues stage
-    // n + 3 of the activations and stage n + 1 of the weights, then waits
-    // until only those eight loads are younger than what it needs (weights
-    // of stage n, issued last step; activations of stage n, older still)
-    // and until its LDS reads of stage n - 1 have returned (that buffer is
-    // the one stage n + 3 overwrites -- the order below keeps the reads of
-    // step n - 1 ahead of the loads of step n).
-    v4i A0[4], A1[4];
+    // Activations run three stages ahead through the LDS ring and weights
+    // three stages ahead through four register sets, issued interleaved
+    // (activations of stage s, then its weights).  Step n first issues stage
+    // n + 3, then waits until only the 24 loads of stages n + 1 .. n + 3 are
+    // outstanding, i.e. stage n has landed, and until its LDS reads of stage
+    // n - 1 have returned (that buffer is the one stage n + 3 overwrites).
+    v4i A[4][4];
     set_tap();
     issue_b(0);
+    load_a(0, A[0]);
     issue_b(1);
+    load_a(1, A[1]);
     issue_b(2);
-    load_a(0, A0);
+    load_a(2, A[2]);
+    auto sub = [&](int n, auto K) __attribute__((always_inline)) {
+        constexpr int k = decltype(K)::value;
+        wait_lgkm0();
+        issue_b(n + 3);
+        load_a(n + 3, A[(k + 3) & 3]);
+        wait_vm<3 * LPS>();
+        step(n, A[k]);
+    };
     int n = 0;
-    for (; n + 2 <= my_steps; n += 2) {
-        wait_lgkm0();
-        issue_b(n + 3);
-        load_a(n + 1, A1);
-        wait_vm<LPS>();
-        step(n, A0);
-        wait_lgkm0();
-        issue_b(n + 4);
-        load_a(n + 2, A0);
-        wait_vm<LPS>();
-        step(n + 1, A1);
+    for (; n + 4 <= my_steps; n += 4) {
+        sub(n, std::integral_constant<int, 0>{});
+        sub(n + 1, std::integral_constant<int, 1>{});
+        sub(n + 2, std::integral_constant<int, 2>{});
+        sub(n + 3, std::integral_constant<int, 3>{});
     }
-    if (n < my_steps) {   // odd step count: the last stage's weights are in A0
-        wait_lgkm0();
-        issue_b(n + 3);
-        load_a(n + 1, A1);
-        wait_vm<LPS>();
-        step(n, A0);
-    }
+    // 1 to 3 remaining steps: their weights are in sets 0, 1, 2
+    if (n < my_steps)
+        sub(n, std::integral_constant<int, 0>{});
+    if (n + 1 < my_steps)
+        sub(n + 1, std::integral_constant<int, 1>{});
+    if (n + 2 < my_steps)
+        sub(n + 2, std::integral_constant<int, 2>{});
     wait_vm<0>();   // trailing out-of-range loads write the ring too
     __syncthreads();
 
@@ -368,18 +381,25 @@ hipError_t launch_frag_pack(const int8_t *wp, int Kpad, int Jpad, int8_t *out, h
 
 int wave_tiles_per_block(int split)
 {
-    return 4 / split;
+    return split > 4 ? 1 : 4 / split;
+}
+
+int wave_threads(int split)
+{
+    return (split > 4 ? split : 4) * 64;
 }
 
 template <int KSPLIT>
 static hipError_t launch_wave_split(const ConvArgs &a, hipStream_t st)
 {
-    const int nwg = (a.ntiles + 4 / KSPLIT - 1) / (4 / KSPLIT);
+    constexpr int TPW = wave_count<KSPLIT>() / KSPLIT;
+    const int nwg = (a.ntiles + TPW - 1) / TPW;
     const int grid = (nwg + 7) / 8 * 8;
+    const dim3 block(wave_count<KSPLIT>() * 64);
     if (a.flip4)
-        hipLaunchKernelGGL((conv_wave_kernel<KSPLIT, 4, true>), dim3(grid), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((conv_wave_kernel<KSPLIT, 4, true>), dim3(grid), block, 0, st, a);
     else
-        hipLaunchKernelGGL((conv_wave_kernel<KSPLIT, 4, false>), dim3(grid), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((conv_wave_kernel<KSPLIT, 4, false>), dim3(grid), block, 0, st, a);
     return hipGetLastError();
 }
 
@@ -388,7 +408,9 @@ hipError_t launch_conv_wave(const ConvArgs &a, int split, hipStream_t st)
     switch (split) {
     case 1: return launch_wave_split<1>(a, st);
     case 2: return launch_wave_split<2>(a, st);
-    default: return launch_wave_split<4>(a, st);
+    case 4: return launch_wave_split<4>(a, st);
+    case 8: return launch_wave_split<8>(a, st);
+    default: return hipErrorInvalidValue;
     }
 }
 

@@ -318,7 +318,7 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
     std::vector<ConvKernel> c;
     const int f_dma = env_int("QNN_DMA", -1), f_tap = env_int("QNN_TAP", -1), f_tile = env_int("QNN_TILE", -1);
     const int f_wave = env_int("QNN_WAVE", -1);
-    if ((f_wave == 1 || f_wave == 2 || f_wave == 4) && dma_ok)
+    if ((f_wave == 1 || f_wave == 2 || f_wave == 4 || f_wave == 8) && dma_ok)
         return {{FAM_WAVE, f_wave}};
     if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok && (!dma_short(f_dma) || (J + 63) / 64 <= dma_stages(f_dma)))
         return {{FAM_DMA, f_dma}};
@@ -327,7 +327,7 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
     if (f_tile >= 0 && f_tile < TILE_COUNT)
         return {{FAM_GATHER, f_tile}};
     if (dma_ok && env_int("QNN_WAVE", -1) != -2)
-        for (int sp : {1, 2, 4})
+        for (int sp : {1, 2, 4, 8})
             if (sp == 1 || J / 64 >= 2 * sp)
                 c.push_back({FAM_WAVE, sp});
     if (tap_ok && env_int("QNN_TAP", -1) != -2)
@@ -925,7 +925,9 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         snprintf(buf, sizeof buf,
                  "%s tile=%dx%dx%d threads=%d stages=%d%s tiles=%d term3=%d border=%d M=%lld K=%d J=%lld cands=%d",
                  fam_name[best.fam], ts.tc, ts.tp, ts.bk,
-                 best.fam == FAM_DMA ? dma_threads(best.tile) : best.fam == FAM_WAVE ? 256 : tap_threads(best.tile),
+                 best.fam == FAM_DMA    ? dma_threads(best.tile)
+                 : best.fam == FAM_WAVE ? wave_threads(best.tile)
+                                        : tap_threads(best.tile),
                  best.fam == FAM_DMA ? dma_stages(best.tile) : best.fam == FAM_WAVE ? 4 : 2,
                  best.fam == FAM_DMA && dma_short(best.tile) ? "s" : "", a.ntiles, (int)term3,
                  (int)ncls, (long long)M, d.K, (long long)Jg, (int)cands.size());

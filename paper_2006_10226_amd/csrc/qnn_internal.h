@@ -186,8 +186,9 @@ int dma_stages(int tile);
 bool dma_short(int tile);   // short-reduction form: at most dma_stages(tile) K-steps
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
 // Wave-independent kernel (conv_wave.hip): 64 x 64 tile per wave, split =
-// 1, 2 or 4 waves sharing a tile's reduction.
+// 1, 2, 4 or 8 waves sharing a tile's reduction (8: 512-thread workgroups).
 hipError_t launch_conv_wave(const ConvArgs &a, int split, hipStream_t st);
+int wave_threads(int split);
 hipError_t launch_frag_pack(const int8_t *wp, int Kpad, int Jpad, int8_t *out, hipStream_t st);
 // corr[c][k] = zp_x * (sum of packed weights of row k over the taps outside
 // the image in border class c: tap (r, s) is inside when bit r of rmask[c]

@@ -59,7 +59,8 @@ def group_of(kernel_name):
         return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * 64} stages={ns}{short}"
     m = _WAVE.search(kernel_name)
     if m:
-        return f"conv_wave tile=64x64x64 threads=256 stages={m.group(2)} split={m.group(1)}"
+        split = int(m.group(1))
+        return f"conv_wave tile=64x64x64 threads={max(4, split) * 64} stages={m.group(2)} split={split}"
     base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
     return base
 

@@ -512,9 +512,9 @@ def test_tuning_file_reuses_the_timed_choice(tmp_path):
         Q.set_tuning_file(None)
 
 
-@pytest.mark.parametrize("split", [1, 2, 4])
+@pytest.mark.parametrize("split", [1, 2, 4, 8])
 def test_every_wave_split(split):
-    """The wave-independent kernel with 1, 2 and 4 waves sharing a tile's
+    """The wave-independent kernel with 1, 2, 4 and 8 waves sharing a tile's
     reduction, forced, on the tap-kernel shapes (ragged tiles, padding,
     strides, int8 input, term 3, int32 output, odd step counts)."""
     with env(QNN_WAVE=split):
