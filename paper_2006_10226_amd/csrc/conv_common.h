@@ -57,7 +57,7 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int v = (int)((uint32_t)acc[e] + (uint32_t)rec[e].y);
-            const int t = (__mulhi(v, rec[e].x) + rec[e].z) >> (rec[e].w - 32);
+            const int t = (__mulhi(v, rec[e].x) + rec[e].z) >> (rec[e].w & 31);   // shift - 32: shift is in [33, 53]
             packed |= (uint32_t)min(max(t, a.lo_off), a.hi_off) << (8 * e);
         }
         return packed ^ a.out_xor;

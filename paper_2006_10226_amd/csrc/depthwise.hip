@@ -173,7 +173,7 @@ __global__ void __launch_bounds__(256) depthwise3_kernel(DwArgs a)
             // 2^(sh-1) + (zp_y + off) 2^sh with sh = shift - 32
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
-                const int t = (__mulhi(v[c], cr[c].mult) + cr[c].rndzp) >> (cr[c].shift - 32);
+                const int t = (__mulhi(v[c], cr[c].mult) + cr[c].rndzp) >> (cr[c].shift & 31);   // shift - 32
                 packed[c >> 2] |= (uint32_t)min(max(t, a.lo_off), a.hi_off) << (8 * (c & 3));
             }
             packed[0] ^= a.out_xor;

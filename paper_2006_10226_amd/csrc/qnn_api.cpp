@@ -140,7 +140,7 @@ enum PlanKind { PLAN_CONV = 0, PLAN_DW = 1, PLAN_REQ = 2 };
 }  // namespace
 
 // One implicit-GEMM kernel configuration: family and tile enum value.
-enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3 };
+enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3, FAM_HALO = 4 };
 struct ConvKernel {
     int fam = FAM_GATHER;
     int tile = TILE_64x64;
@@ -300,6 +300,7 @@ TileShape kernel_shape(const ConvKernel &k)
 {
     switch (k.fam) {
     case FAM_WAVE: return {64, 64, 64};
+    case FAM_HALO: return {64, 64, 64};
     case FAM_DMA: return dma_tile_shape(k.tile);
     case FAM_TAP: return tap_tile_shape(k.tile);
     default: return tile_shape(k.tile);
@@ -363,9 +364,14 @@ void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr
     a.pcorr = zero_pad ? pcorr_tab : nullptr;
     a.pcls = zero_pad ? pcls_tab : nullptr;
     const int64_t tiles_c = (a.K + ts.tc - 1) / ts.tc;
-    const int64_t ntiles = tiles_c * (((int64_t)a.M + ts.tp - 1) / ts.tp);
+    int64_t ntiles = tiles_c * (((int64_t)a.M + ts.tp - 1) / ts.tp);
+    if (k.fam == FAM_HALO) {
+        // one wave tile is whole output rows of one image
+        const long long tp = halo_pixel_tiles(a);
+        ntiles = tp < 0 ? -1 : tiles_c * tp;
+    }
     a.tiles_c = (int)tiles_c;
-    a.ntiles = ntiles < (int64_t(1) << 31) - 8 ? (int)ntiles : -1;
+    a.ntiles = ntiles >= 0 && ntiles < (int64_t(1) << 31) - 8 ? (int)ntiles : -1;
     a.nk = (a.J + ts.bk - 1) / ts.bk;
     a.nblocks = 0;
     if (k.fam == FAM_GATHER && a.ntiles >= 0) {
@@ -381,6 +387,7 @@ hipError_t launch_conv_kernel(const ConvArgs &a, const ConvKernel &k, int avec, 
 {
     switch (k.fam) {
     case FAM_WAVE: return launch_conv_wave(a, k.tile, st);
+    case FAM_HALO: return launch_conv_halo(a, k.tile, st);
     case FAM_DMA: return launch_conv_dma(a, k.tile, st);
     case FAM_TAP: return launch_conv_tap(a, k.tile, st);
     default: return launch_conv(a, k.tile, avec, st);
@@ -424,11 +431,12 @@ qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &ca
             if (a.ntiles < 0)
                 continue;
             float t = 0;
-            // one untimed launch, then the median of three cold launches
+            // one untimed launch, then the median of five cold launches
             if ((e = launch_conv_kernel(a, k, avec, st)) != hipSuccess)
                 break;
-            float runs[3];
-            for (int r = 0; r < 3 && e == hipSuccess; ++r) {
+            constexpr int kRuns = 5;
+            float runs[kRuns];
+            for (int r = 0; r < kRuns && e == hipSuccess; ++r) {
                 if (flush && (e = hipMemsetAsync(flush, r, flush_bytes, st)) != hipSuccess)
                     break;
                 if ((e = hipEventRecord(e0, st)) != hipSuccess || (e = launch_conv_kernel(a, k, avec, st)) != hipSuccess ||
@@ -438,8 +446,8 @@ qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &ca
             }
             if (e != hipSuccess)
                 break;
-            std::sort(runs, runs + 3);
-            t = runs[1];
+            std::sort(runs, runs + kRuns);
+            t = runs[kRuns / 2];
             if (t < best_ms) {
                 best_ms = t;
                 *best = k;
@@ -580,6 +588,21 @@ bool border_classes(const ConvDesc &d, int Ho, int Wo, int64_t M, BorderClasses 
             for (int ow = 0; ow < Wo; ++ow)
                 bc.pcls[m++] = id[(size_t)rcls[oh] * cu.size() + ccls[ow]];
     return true;
+}
+
+// LDS bytes one workgroup may use on the current device.
+int device_lds_per_block()
+{
+    static int bytes = 0;
+    if (!bytes) {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && n > 0)
+            bytes = n;
+        else
+            bytes = 64 * 1024;
+    }
+    return bytes;
 }
 
 int device_cus()
@@ -893,6 +916,28 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     }
     p->ws_bytes = p->ws_asum_bytes + p->ws_xpad_bytes;
 
+    // the window kernel joins the candidates of the shapes it serves when
+    // its LDS fits; QNN_HALO=4|8 forces it (if eligible), -2 leaves it out
+    if (!rowpack && dma_ok) {
+        const int f_halo = env_int("QNN_HALO", -1);
+        const int f_wave = env_int("QNN_WAVE", -1);
+        const bool other_forced = env_int("QNN_DMA", -1) >= 0 || env_int("QNN_TAP", -1) >= 0 ||
+                                  env_int("QNN_TILE", -1) >= 0 ||
+                                  f_wave == 1 || f_wave == 2 || f_wave == 4 || f_wave == 8;
+        std::vector<ConvKernel> hk;
+        for (int nw : {8, 4}) {
+            const size_t lds = halo_lds_bytes(a, nw);
+            if (lds && lds <= (size_t)device_lds_per_block() && (f_halo < 0 || f_halo == nw))
+                hk.push_back({FAM_HALO, nw});
+        }
+        if (f_halo == 4 || f_halo == 8) {
+            if (!hk.empty())
+                cands = hk;
+        } else if (f_halo != -2 && !other_forced) {
+            cands.insert(cands.end(), hk.begin(), hk.end());
+        }
+    }
+
     // kernel choice: the candidates are timed on this very shape (the
     // weights and tables are real, the activations a constant fill) and
     // the fastest is kept; every candidate computes the same bytes
@@ -914,7 +959,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
     }
     const TileShape ts = kernel_shape(best);
-    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave"};
+    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave", "conv_halo"};
     char buf[200];
     if (best.fam == FAM_GATHER)
         snprintf(buf, sizeof buf,
@@ -927,8 +972,9 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
                  fam_name[best.fam], ts.tc, ts.tp, ts.bk,
                  best.fam == FAM_DMA    ? dma_threads(best.tile)
                  : best.fam == FAM_WAVE ? wave_threads(best.tile)
+                 : best.fam == FAM_HALO ? best.tile * 64
                                         : tap_threads(best.tile),
-                 best.fam == FAM_DMA ? dma_stages(best.tile) : best.fam == FAM_WAVE ? 4 : 2,
+                 best.fam == FAM_DMA ? dma_stages(best.tile) : best.fam == FAM_WAVE ? 4 : best.fam == FAM_HALO ? 1 : 2,
                  best.fam == FAM_DMA && dma_short(best.tile) ? "s" : "", a.ntiles, (int)term3,
                  (int)ncls, (long long)M, d.K, (long long)Jg, (int)cands.size());
     if (best.fam == FAM_WAVE) {
@@ -1379,7 +1425,7 @@ qnn_status qnn_set_tuning_file(const char *path)
             char key[256];
             int fam = 0, tile = 0;
             while (std::fscanf(f, "%255s %d %d", key, &fam, &tile) == 3)
-                if (fam >= FAM_GATHER && fam <= FAM_WAVE && tile >= 0)
+                if (fam >= FAM_GATHER && fam <= FAM_HALO && tile >= 0)
                     rec[key] = ConvKernel{fam, tile};
             std::fclose(f);
         }

@@ -189,6 +189,15 @@ hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
 // 1, 2, 4 or 8 waves sharing a tile's reduction (8: 512-thread workgroups).
 hipError_t launch_conv_wave(const ConvArgs &a, int split, hipStream_t st);
 int wave_threads(int split);
+// Window kernel (conv_halo.hip): stride 1, undilated 3x3, C % 64 == 0,
+// Wo <= 64; nw = 4 or 8 waves per workgroup, each computing whole output
+// rows of one image for 64 channels from an LDS copy of their input window,
+// the workgroup's weights resident in LDS.  halo_lds_bytes: dynamic LDS of
+// a launch, 0 when the shape is not eligible; halo_pixel_tiles: wave tiles
+// per 64-channel tile, -1 when not eligible.
+size_t halo_lds_bytes(const ConvArgs &a, int nw);
+long long halo_pixel_tiles(const ConvArgs &a);
+hipError_t launch_conv_halo(const ConvArgs &a, int nw, hipStream_t st);
 hipError_t launch_frag_pack(const int8_t *wp, int Kpad, int Jpad, int8_t *out, hipStream_t st);
 // corr[c][k] = zp_x * (sum of packed weights of row k over the taps outside
 // the image in border class c: tap (r, s) is inside when bit r of rmask[c]

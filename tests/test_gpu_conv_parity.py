@@ -553,3 +553,82 @@ def test_row_pair_mode(layer, N):
             with env(**cfg):
                 got = run_gpu(c)
             assert_equal(got, run_oracle(c), f"{layer.name} {cfg} {kw}: {d}")
+
+
+# Stride-1 3x3 layers of the window kernel (conv_halo.hip), forced with 4
+# and 8 waves per workgroup where its LDS fits: one and two 64-channel
+# slices, whole-row tiles of 1 to 7 rows with a short last band, a 64-pixel
+# row, ragged and several channel tiles, asymmetric and no padding, int8
+# input and output, weight zero points, int32 output, half-away rounding.
+HALO_SHAPES = [
+    (W.ConvLayer("h56", 56, 56, 64, 64, 3, 3, 1, (1, 1, 1, 1)), 2, {}),
+    (W.ConvLayer("h28", 28, 28, 128, 128, 3, 3, 1, (1, 1, 1, 1)), 2, {}),
+    (W.ConvLayer("h13", 13, 13, 64, 96, 3, 3, 1, (1, 1, 1, 1)), 3, {}),
+    (W.ConvLayer("h64", 9, 64, 64, 72, 3, 3, 1, (1, 1, 1, 1)), 2, dict(x_dtype="i8")),
+    (W.ConvLayer("hpad", 12, 10, 64, 64, 3, 3, 1, (0, 2, 1, 0)), 3, dict(yt="i8")),
+    (W.ConvLayer("hnopad", 10, 11, 128, 80, 3, 3, 1, (0, 0, 0, 0)), 2, dict(zp_w="channel")),
+    (W.ConvLayer("h1", 1, 1, 64, 64, 3, 3, 1, (1, 1, 1, 1)), 4, dict(yt="i32")),
+    (W.ConvLayer("h7", 7, 7, 64, 300, 3, 3, 1, (1, 1, 1, 1)), 3, dict(rounding="half_away")),
+]
+
+
+def _halo_lds(layer, nw):
+    """LDS bytes of a window-kernel launch: resident weights (R*S*C/64
+    fragments of 4 KB), 64 channel records, the workgroup's input window
+    (nw bands of tr output rows plus 2 rows, Wo + 2 columns, 64 bytes per
+    cell and channel slice, in 1 KB loads), whose space later holds a 64 x
+    80 byte staging tile per wave."""
+    pt, pl, pb, pr = layer.pads
+    Ho, Wo = layer.H + pt + pb - 2, layer.W + pl + pr - 2
+    tr = min(Ho, 64 // Wo)
+    bands = -(-Ho // tr)
+    rows = min(bands, nw) * tr + 2
+    ninst = -(-(rows * (Wo + 2)) // 16)
+    return 9 * layer.Cin // 64 * 4096 + 1024 + max(layer.Cin // 64 * ninst * 1024, nw * 64 * 80)
+
+
+@pytest.mark.parametrize("nw", [4, 8])
+def test_every_halo_config(nw):
+    ran = 0
+    for i, (layer, N, kw) in enumerate(HALO_SHAPES):
+        c = W.conv_case(layer, N, seed=700 + nw * 10 + i, **kw)
+        with env(QNN_HALO=nw):
+            p, keep = make_plan(c)
+            d = p.describe()
+            p.close()
+            if not d.startswith("conv_halo"):
+                assert _halo_lds(layer, nw) > 160 * 1024, d
+                continue
+            assert f"threads={nw * 64}" in d, d
+            log(f"halo nw {nw} shape {layer.name}: {d}")
+            assert_equal(run_gpu(c), run_oracle(c), f"halo nw {nw} {layer.name} {kw}")
+            ran += 1
+    assert ran >= 5
+    # zero point 0: no padding correction table
+    c = W.conv_case(HALO_SHAPES[2][0], 2, seed=9)
+    c.zp_x = 0
+    with env(QNN_HALO=nw):
+        assert_equal(run_gpu(c), run_oracle(c), f"halo nw {nw} zp_x 0")
+
+
+@pytest.mark.parametrize("coff", [8, 64])
+def test_halo_channel_slice_output(coff):
+    """Window kernel writing a channel slice of a wider output: staged
+    16-byte chunks when aligned, direct stores otherwise; bytes outside the
+    slice stay untouched."""
+    layer = W.ConvLayer("hslice", 12, 13, 64, 72, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 3, seed=33)
+    total = 160
+    with env(QNN_HALO=8):
+        p, keep = make_plan(c, y_ldc=total, y_coff=coff)
+        d = p.describe()
+        assert d.startswith("conv_halo"), d
+        out = torch.full((3, 12, 13, total), 77, dtype=torch.uint8, device="cuda")
+        p.run(dev(c.x), out=out)
+        torch.cuda.synchronize()
+        p.close()
+    y = out.cpu().numpy()
+    assert_equal(y[..., coff:coff + 72], run_oracle(c), f"halo slice {coff}")
+    rest = np.ones(total, bool)
+    rest[coff:coff + 72] = False
+    assert (y[..., rest] == 77).all()
