@@ -26,6 +26,7 @@ _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\
 _TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
 _DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)>")
 _WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
+_HALO = re.compile(r"conv_halo_kernel<(\d+), ?(true|false)>")
 
 
 def kernel_source_sha1(root=None):
@@ -61,6 +62,9 @@ def group_of(kernel_name):
     if m:
         split = int(m.group(1))
         return f"conv_wave tile=64x64x64 threads={max(4, split) * 64} stages={m.group(2)} split={split}"
+    m = _HALO.search(kernel_name)
+    if m:
+        return f"conv_halo tile=64x64x64 threads={int(m.group(1)) * 64} stages=1"
     base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
     return base
 
