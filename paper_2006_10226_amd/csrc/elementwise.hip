@@ -315,4 +315,25 @@ hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned,
     return hipGetLastError();
 }
 
+// Reads n16 16-byte words of `buf` (grid-stride) so that the L2s and the
+// last-level cache hold clean lines of it; `sink` receives a value only in
+// the impossible case of an all-ones sum, which keeps the loads alive.
+__global__ void __launch_bounds__(256) cache_sweep_kernel(const uint4 *buf, long long n16, int *sink)
+{
+    uint32_t acc = 0;
+    for (long long i = blockIdx.x * 256LL + threadIdx.x; i < n16; i += (long long)gridDim.x * 256) {
+        const uint4 v = buf[i];
+        acc += v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0xffffffffu)
+        *sink = (int)acc;
+}
+
+hipError_t launch_cache_sweep(const void *buf, size_t bytes, int *sink, hipStream_t st)
+{
+    hipLaunchKernelGGL(cache_sweep_kernel, dim3(4096), dim3(256), 0, st, (const uint4 *)buf, (long long)(bytes / 16),
+                       sink);
+    return hipGetLastError();
+}
+
 }  // namespace qnn

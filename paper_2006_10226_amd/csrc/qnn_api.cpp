@@ -409,12 +409,23 @@ qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &ca
     if (e != hipSuccess)
         return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes for kernel tuning failed", xb + yb + sb);
     // Each timed launch starts with cold caches, as a layer does inside a
-    // network: a fill larger than the L2s and the 256 MB last-level cache
+    // network: a pass over more than the L2s and the 256 MB last-level cache
     // runs before it.  (Without the buffer the timing is warm.)
     const size_t flush_bytes = size_t(320) << 20;
     void *flush = nullptr;
     if (hipMalloc(&flush, flush_bytes) != hipSuccess)
         flush = nullptr;
+    // The eviction reads the whole buffer through the caches, then writes 16
+    // MB of it: the caches then hold clean lines plus some dirty ones, as a
+    // layer inside the stack finds them after its predecessor's output.
+    // QNN_TUNE_FLUSH=0 fills the whole buffer instead (all lines dirty).
+    const bool sweep = env_int("QNN_TUNE_FLUSH", 1) != 0;
+    auto evict = [&](int r) -> hipError_t {
+        if (!sweep)
+            return hipMemsetAsync(flush, r, flush_bytes, st);
+        hipError_t er = launch_cache_sweep(flush, flush_bytes, (int *)buf, st);
+        return er != hipSuccess ? er : hipMemsetAsync(flush, r, size_t(16) << 20, st);
+    };
     hipEvent_t e0 = nullptr, e1 = nullptr;
     qnn_status s = QNN_OK;
     float best_ms = 1e30f;
@@ -437,7 +448,7 @@ qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &ca
             constexpr int kRuns = 5;
             float runs[kRuns];
             for (int r = 0; r < kRuns && e == hipSuccess; ++r) {
-                if (flush && (e = hipMemsetAsync(flush, r, flush_bytes, st)) != hipSuccess)
+                if (flush && (e = evict(r)) != hipSuccess)
                     break;
                 if ((e = hipEventRecord(e0, st)) != hipSuccess || (e = launch_conv_kernel(a, k, avec, st)) != hipSuccess ||
                     (e = hipEventRecord(e1, st)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess ||

@@ -233,6 +233,9 @@ hipError_t launch_prep_dw3(const int8_t *w, const int32_t *bias, int C, int32_t 
 hipError_t launch_depthwise3(const DwArgs &a, hipStream_t st);
 int dw3_pixels();   // output pixels along a row per work item of launch_depthwise3
 hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, hipStream_t st);
+// Reads `bytes` (a multiple of 16) of `buf` through the caches (kernel
+// tuning uses it to evict what a timed launch would otherwise find cached).
+hipError_t launch_cache_sweep(const void *buf, size_t bytes, int *sink, hipStream_t st);
 hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned, hipStream_t st);
 
 }  // namespace qnn
