@@ -141,6 +141,8 @@ def kernel_group(it):
     extra = f"gather={d['gather']}" if "gather" in d else f"threads={d['threads']} stages={d.get('stages', '')}"
     if "split" in d:
         extra += f" split={d['split']}"
+    if "cfg" in d:
+        extra += f" cfg={d['cfg']}"
     return f"{words[0]} tile={d['tile']} {extra}"
 
 

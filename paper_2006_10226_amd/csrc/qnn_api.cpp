@@ -140,7 +140,7 @@ enum PlanKind { PLAN_CONV = 0, PLAN_DW = 1, PLAN_REQ = 2 };
 }  // namespace
 
 // One implicit-GEMM kernel configuration: family and tile enum value.
-enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3, FAM_HALO = 4 };
+enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3, FAM_HALO = 4, FAM_WIN = 5 };
 struct ConvKernel {
     int fam = FAM_GATHER;
     int tile = TILE_64x64;
@@ -301,6 +301,7 @@ TileShape kernel_shape(const ConvKernel &k)
     switch (k.fam) {
     case FAM_WAVE: return {64, 64, 64};
     case FAM_HALO: return {64, 64, 64};
+    case FAM_WIN: return {win_channels(k.tile), 64, 64};
     case FAM_DMA: return dma_tile_shape(k.tile);
     case FAM_TAP: return tap_tile_shape(k.tile);
     default: return tile_shape(k.tile);
@@ -369,6 +370,9 @@ void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr
         // one wave tile is whole output rows of one image
         const long long tp = halo_pixel_tiles(a);
         ntiles = tp < 0 ? -1 : tiles_c * tp;
+    } else if (k.fam == FAM_WIN) {
+        const long long wg = win_workgroups_per_ctile(a, k.tile);
+        ntiles = wg < 0 ? -1 : tiles_c * wg;
     }
     a.tiles_c = (int)tiles_c;
     a.ntiles = ntiles >= 0 && ntiles < (int64_t(1) << 31) - 8 ? (int)ntiles : -1;
@@ -388,6 +392,7 @@ hipError_t launch_conv_kernel(const ConvArgs &a, const ConvKernel &k, int avec, 
     switch (k.fam) {
     case FAM_WAVE: return launch_conv_wave(a, k.tile, st);
     case FAM_HALO: return launch_conv_halo(a, k.tile, st);
+    case FAM_WIN: return launch_conv_window(a, k.tile, st);
     case FAM_DMA: return launch_conv_dma(a, k.tile, st);
     case FAM_TAP: return launch_conv_tap(a, k.tile, st);
     default: return launch_conv(a, k.tile, avec, st);
@@ -947,6 +952,21 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         } else if (f_halo != -2 && !other_forced) {
             cands.insert(cands.end(), hk.begin(), hk.end());
         }
+        // the streaming window kernel likewise: QNN_WIN=<cfg> forces one
+        // configuration (if eligible), -2 leaves the family out
+        const int f_win = env_int("QNN_WIN", -1);
+        std::vector<ConvKernel> wk;
+        for (int c = 0; c < win_count(); ++c) {
+            const size_t lds = win_lds_bytes(a, c);
+            if (lds && lds <= (size_t)device_lds_per_block() && (f_win < 0 || f_win == c))
+                wk.push_back({FAM_WIN, c});
+        }
+        if (f_win >= 0) {
+            if (!wk.empty())
+                cands = wk;
+        } else if (f_win != -2 && f_halo < 0 && !other_forced) {
+            cands.insert(cands.end(), wk.begin(), wk.end());
+        }
     }
 
     // kernel choice: the candidates are timed on this very shape (the
@@ -970,7 +990,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
         return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
     }
     const TileShape ts = kernel_shape(best);
-    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave", "conv_halo"};
+    static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave", "conv_halo", "conv_window"};
     char buf[200];
     if (best.fam == FAM_GATHER)
         snprintf(buf, sizeof buf,
@@ -984,6 +1004,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
                  best.fam == FAM_DMA    ? dma_threads(best.tile)
                  : best.fam == FAM_WAVE ? wave_threads(best.tile)
                  : best.fam == FAM_HALO ? best.tile * 64
+                 : best.fam == FAM_WIN  ? win_threads(best.tile)
                                         : tap_threads(best.tile),
                  best.fam == FAM_DMA ? dma_stages(best.tile) : best.fam == FAM_WAVE ? 4 : best.fam == FAM_HALO ? 1 : 2,
                  best.fam == FAM_DMA && dma_short(best.tile) ? "s" : "", a.ntiles, (int)term3,
@@ -991,6 +1012,9 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     if (best.fam == FAM_WAVE) {
         const size_t n = strlen(buf);
         snprintf(buf + n, sizeof buf - n, " split=%d", best.tile);
+    } else if (best.fam == FAM_WIN) {
+        const size_t n = strlen(buf);
+        snprintf(buf + n, sizeof buf - n, " cfg=%d", best.tile);
     }
     p->desc = buf;
     *out = p;
@@ -1436,7 +1460,7 @@ qnn_status qnn_set_tuning_file(const char *path)
             char key[256];
             int fam = 0, tile = 0;
             while (std::fscanf(f, "%255s %d %d", key, &fam, &tile) == 3)
-                if (fam >= FAM_GATHER && fam <= FAM_HALO && tile >= 0)
+                if (fam >= FAM_GATHER && fam <= FAM_WIN && tile >= 0)
                     rec[key] = ConvKernel{fam, tile};
             std::fclose(f);
         }

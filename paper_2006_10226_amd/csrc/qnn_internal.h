@@ -198,6 +198,16 @@ int wave_threads(int split);
 size_t halo_lds_bytes(const ConvArgs &a, int nw);
 long long halo_pixel_tiles(const ConvArgs &a);
 hipError_t launch_conv_halo(const ConvArgs &a, int nw, hipStream_t st);
+// Streaming window kernel (conv_window.hip): stride 1, undilated 3x3,
+// C % 64 == 0, Wo <= 64; the input window of a workgroup's bands stays in
+// LDS while the weights stream through it.  cfg indexes its configurations
+// (bands per workgroup, reduction split, channels per workgroup).
+int win_count();
+int win_channels(int cfg);
+int win_threads(int cfg);
+size_t win_lds_bytes(const ConvArgs &a, int cfg);               // 0: not eligible
+long long win_workgroups_per_ctile(const ConvArgs &a, int cfg);  // -1: not eligible
+hipError_t launch_conv_window(const ConvArgs &a, int cfg, hipStream_t st);
 hipError_t launch_frag_pack(const int8_t *wp, int Kpad, int Jpad, int8_t *out, hipStream_t st);
 // corr[c][k] = zp_x * (sum of packed weights of row k over the taps outside
 // the image in border class c: tap (r, s) is inside when bit r of rmask[c]

@@ -27,6 +27,9 @@ _TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
 _DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)>")
 _WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
 _HALO = re.compile(r"conv_halo_kernel<(\d+), ?(true|false)>")
+_WIN = re.compile(r"conv_window_kernel<(\d+), ?(\d+), ?(\d+), ?(true|false)>")
+# streaming window configurations (bands, reduction split, 16-channel blocks), in plan tile order
+_WIN_CFGS = [(4, 2, 2), (2, 2, 2), (4, 1, 2), (8, 1, 2)]
 
 
 def kernel_source_sha1(root=None):
@@ -65,6 +68,11 @@ def group_of(kernel_name):
     m = _HALO.search(kernel_name)
     if m:
         return f"conv_halo tile=64x64x64 threads={int(m.group(1)) * 64} stages=1"
+    m = _WIN.search(kernel_name)
+    if m:
+        nb, ks, tcb = (int(v) for v in m.groups()[:3])
+        cfg = _WIN_CFGS.index((nb, ks, tcb)) if (nb, ks, tcb) in _WIN_CFGS else -1
+        return f"conv_window tile={16 * tcb}x64x64 threads={nb * ks * 64} stages=2 cfg={cfg}"
     base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
     return base
 

@@ -632,3 +632,80 @@ def test_halo_channel_slice_output(coff):
     rest = np.ones(total, bool)
     rest[coff:coff + 72] = False
     assert (y[..., rest] == 77).all()
+
+
+# Stride-1 3x3 layers of the streaming window kernel (conv_window.hip),
+# every configuration forced where its LDS fits: bands shared within an
+# image and whole-image bands (batch not a multiple of the bands per
+# workgroup), one to eight channel slices (a partial last slice group),
+# ragged and several channel tiles, asymmetric and no padding, int8 input
+# and output, weight zero points, int32 output, half-away rounding.
+WIN_SHAPES = [
+    (W.ConvLayer("w14", 14, 14, 256, 256, 3, 3, 1, (1, 1, 1, 1)), 3, {}),
+    (W.ConvLayer("w7", 7, 7, 512, 200, 3, 3, 1, (1, 1, 1, 1)), 5, {}),
+    (W.ConvLayer("w13", 13, 13, 192, 96, 3, 3, 1, (1, 1, 1, 1)), 2, dict(x_dtype="i8")),
+    (W.ConvLayer("wpad", 12, 10, 128, 64, 3, 3, 1, (0, 2, 1, 0)), 3, dict(yt="i8")),
+    (W.ConvLayer("wnopad", 10, 11, 320, 80, 3, 3, 1, (0, 0, 0, 0)), 2, dict(zp_w="channel")),
+    (W.ConvLayer("w1", 1, 1, 64, 48, 3, 3, 1, (1, 1, 1, 1)), 5, dict(yt="i32")),
+    (W.ConvLayer("w28", 28, 28, 128, 40, 3, 3, 1, (1, 1, 1, 1)), 2, dict(rounding="half_away")),
+]
+WIN_CFGS = [(4, 2, 2), (2, 2, 2), (4, 1, 2), (8, 1, 2)]
+
+
+def _win_lds(layer, cfg):
+    """LDS bytes of a streaming-window launch: two weight groups (KS slices
+    x 9 taps x TCB 1 KB fragments; the partial sums and 1 KB of channel
+    records reuse them), the window (the staging tiles reuse it)."""
+    nb, ks, tcb = WIN_CFGS[cfg]
+    pt, pl, pb, pr = layer.pads
+    Ho, Wo = layer.H + pt + pb - 2, layer.W + pl + pr - 2
+    tr = min(Ho, 64 // Wo)
+    bands = -(-Ho // tr)
+    rows = nb * (Ho + 2) if bands == 1 else min(bands, nb) * tr + 2
+    ninst = -(-(rows * (Wo + 2)) // 16)
+    wgt = max(2 * tcb * ks * 9 * 1024, nb * (ks - 1) * tcb * 4 * 1024 + 1024)
+    return wgt + max(layer.Cin // 64 * ninst * 1024, nb * 64 * (16 * tcb + 16))
+
+
+@pytest.mark.parametrize("cfg", range(len(WIN_CFGS)))
+def test_every_window_config(cfg):
+    ran = 0
+    for i, (layer, N, kw) in enumerate(WIN_SHAPES):
+        c = W.conv_case(layer, N, seed=800 + cfg * 10 + i, **kw)
+        with env(QNN_WIN=cfg):
+            p, keep = make_plan(c)
+            d = p.describe()
+            p.close()
+            if not d.startswith("conv_window"):
+                assert _win_lds(layer, cfg) > 160 * 1024, d
+                continue
+            assert d.endswith(f"cfg={cfg}"), d
+            log(f"window cfg {cfg} shape {layer.name}: {d}")
+            assert_equal(run_gpu(c), run_oracle(c), f"window cfg {cfg} {layer.name} {kw}")
+            ran += 1
+    assert ran >= 4
+    c = W.conv_case(WIN_SHAPES[2][0], 2, seed=10)
+    c.zp_x = 0
+    with env(QNN_WIN=cfg):
+        assert_equal(run_gpu(c), run_oracle(c), f"window cfg {cfg} zp_x 0")
+
+
+@pytest.mark.parametrize("coff", [8, 64])
+def test_window_channel_slice_output(coff):
+    """Streaming window kernel writing a channel slice of a wider output."""
+    layer = W.ConvLayer("wslice", 12, 13, 128, 72, 3, 3, 1, (1, 1, 1, 1))
+    c = W.conv_case(layer, 3, seed=34)
+    total = 160
+    with env(QNN_WIN=0):
+        p, keep = make_plan(c, y_ldc=total, y_coff=coff)
+        d = p.describe()
+        assert d.startswith("conv_window"), d
+        out = torch.full((3, 12, 13, total), 77, dtype=torch.uint8, device="cuda")
+        p.run(dev(c.x), out=out)
+        torch.cuda.synchronize()
+        p.close()
+    y = out.cpu().numpy()
+    assert_equal(y[..., coff:coff + 72], run_oracle(c), f"window slice {coff}")
+    rest = np.ones(total, bool)
+    rest[coff:coff + 72] = False
+    assert (y[..., rest] == 77).all()
