@@ -247,21 +247,25 @@ def cpu_baseline(workload, target_s=12.0):
 
 # ------------------------------------------------------------------ traffic from committed counters
 
-def traffic_for(group):
+def traffic_for(group, workload):
     """HBM bytes per launch of the dominant kernel from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, if it was taken on the current
-    kernel source (else None)."""
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary of this workload
+    (profiles/traffic_<workload>.json, or profiles/traffic.json when it
+    names the workload), if it was taken on the current kernel source (else
+    None)."""
     from paper_2006_10226_amd.rocprof_summary import kernel_source_sha1
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
-        return None
-    try:
-        rec = json.load(open(path))
-        if rec.get("source_sha1") != kernel_source_sha1(ROOT):
+    for name in (f"traffic_{workload}.json", "traffic.json"):
+        path = os.path.join(ROOT, "profiles", name)
+        if not os.path.exists(path):
+            continue
+        try:
+            rec = json.load(open(path))
+            if rec.get("workload") != workload or rec.get("source_sha1") != kernel_source_sha1(ROOT):
+                return None
+            return rec.get("groups", {}).get(group, {}).get("bytes_per_launch")
+        except Exception:
             return None
-        return rec.get("groups", {}).get(group, {}).get("bytes_per_launch")
-    except Exception:
-        return None
+    return None
 
 
 def main():
@@ -342,7 +346,7 @@ def main():
         achieved = D["bytes"] / D["launches"] / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = traffic_for(dom)
+    roof["traffic"] = traffic_for(dom, args.workload)
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_ms * 1e3, 3)
     roof["avg_launch_us_event_bracketed"] = round(D["ms"] / D["launches"] * 1e3, 3)

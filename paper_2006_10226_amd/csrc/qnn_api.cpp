@@ -776,8 +776,11 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     // row-pair mode of the LDS-direct kernel for small channel counts (the
     // 3-channel stems): two filter rows of S * C4 <= 32 bytes per K-step,
     // over a zero-point padded copy of the image
+    // (1x1 convolutions whose pixels are whole 16-byte chunks gather them
+    // directly: the padded copy would only cost a pass over x)
+    const bool whole_chunks_1x1 = d.R == 1 && d.S == 1 && C4 % 16 == 0;
     const bool rowpack = !tap_ok && C4 * d.S <= 32 && d.R <= 32 && d.cp.dil_h == 1 && d.cp.dil_w == 1 && !term3 &&
-                         env_int("QNN_ROWPACK", 1) != 0 && env_int("QNN_TILE", -1) < 0;
+                         !whole_chunks_1x1 && env_int("QNN_ROWPACK", 1) != 0 && env_int("QNN_TILE", -1) < 0;
     const int npairs = (d.R + 1) / 2;
     const int Jr = npairs * 64;                      // row-pair reduction length
     const int Hp = std::max(d.H + d.cp.pad_top + d.cp.pad_bottom, (Ho - 1) * d.cp.stride_h + 2 * npairs);
