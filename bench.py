@@ -337,8 +337,13 @@ def main():
     # graph-timed step, gives its average kernel duration.
     scale = ms / float(np.sum(per))
     avg_ms = D["ms"] * scale / D["launches"]
-    if D["macs"] > 0 and dom.startswith("conv_"):
-        # conv and dense run on the matrix cores
+    # the group's bound is the lower of its two roofs: a conv or dense group
+    # whose algorithmic ops per byte sit above the ridge (peak ops / peak
+    # bytes) is bound by the matrix cores, below it by HBM (as depthwise,
+    # requantize and add always are)
+    ridge = PEAK_INT8_TOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    mfma_bound = D["macs"] > 0 and dom.startswith("conv_") and 2.0 * D["macs"] / max(D["bytes"], 1) >= ridge
+    if mfma_bound:
         achieved = 2.0 * D["macs"] / D["launches"] / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": round(achieved / PEAK_INT8_TOPS, 4)}
