@@ -312,29 +312,35 @@ int device_cus();
 
 // Candidate kernels for a conv of M pixels x K channels with C4 channels
 // per tap and reduction J.  QNN_DMA / QNN_TAP / QNN_TILE=<n> force one
-// configuration when it is eligible (for sweeps and tests).
-std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool tap_ok, bool dma_ok)
+// configuration when it is eligible (for sweeps and tests).  one_tap: a
+// 1x1 filter, whose K-steps may end past the pixel's channels (C4 % 16 ==
+// 0): the extra bytes are the next pixels' and meet zero weights.
+std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool tap_ok, bool dma_ok, bool one_tap)
 {
     (void)M;
     (void)K;
     std::vector<ConvKernel> c;
     const int f_dma = env_int("QNN_DMA", -1), f_tap = env_int("QNN_TAP", -1), f_tile = env_int("QNN_TILE", -1);
     const int f_wave = env_int("QNN_WAVE", -1);
-    if ((f_wave == 1 || f_wave == 2 || f_wave == 4 || f_wave == 8) && dma_ok)
+    // the wave kernel starts its split reduction at tap (ks / (C / 64)):
+    // whole 64-channel steps only
+    const bool wave_ok = dma_ok && C4 % 64 == 0;
+    auto tap_fits = [&](int t) { return C4 % tap_tile_shape(t).bk == 0 || one_tap; };
+    if ((f_wave == 1 || f_wave == 2 || f_wave == 4 || f_wave == 8) && wave_ok)
         return {{FAM_WAVE, f_wave}};
     if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok && (!dma_short(f_dma) || (J + 63) / 64 <= dma_stages(f_dma)))
         return {{FAM_DMA, f_dma}};
-    if (f_tap >= 0 && f_tap < TAP_COUNT && tap_ok && C4 % tap_tile_shape(f_tap).bk == 0)
+    if (f_tap >= 0 && f_tap < TAP_COUNT && tap_ok && tap_fits(f_tap))
         return {{FAM_TAP, f_tap}};
     if (f_tile >= 0 && f_tile < TILE_COUNT)
         return {{FAM_GATHER, f_tile}};
-    if (dma_ok && env_int("QNN_WAVE", -1) != -2)
+    if (wave_ok && env_int("QNN_WAVE", -1) != -2)
         for (int sp : {1, 2, 4, 8})
             if (sp == 1 || J / 64 >= 2 * sp)
                 c.push_back({FAM_WAVE, sp});
     if (tap_ok && env_int("QNN_TAP", -1) != -2)
         for (int t = 0; t < TAP_COUNT; ++t)
-            if (C4 % tap_tile_shape(t).bk == 0)
+            if (tap_fits(t))
                 c.push_back({FAM_TAP, t});
     if (dma_ok && env_int("QNN_DMA", -1) != -2) {
         for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_256x128_S4, DMA_128x256_S4,
@@ -345,11 +351,14 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
             if ((J + 63) / 64 <= dma_stages(t))
                 c.push_back({FAM_DMA, t});
     }
-    if (c.empty()) {
-        // the general gather kernel: short reductions use the 64-deep K-step
+    if (c.empty() || C4 % 64 != 0) {
+        // the general gather kernel (short reductions use the 64-deep
+        // K-step); for 1x1 filters with partial K-steps it competes with
+        // the tap-walk kernels, which read up to 48 bytes past each pixel
+        const size_t first = c.size();
         c.push_back({FAM_GATHER, J <= 64 ? TILE_64x64_K64 : TILE_64x64});
         for (int t : {TILE_64x64_K64, TILE_64x128, TILE_128x64, TILE_128x128})
-            if (t != c[0].tile)
+            if (t != c[first].tile)
                 c.push_back({FAM_GATHER, t});
     }
     return c;
@@ -772,15 +781,16 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
                 return true;
         return false;
     }();
-    const bool tap_ok = C4 % 64 == 0 && d.R <= 16 && d.S <= 16;
+    // tap-walk kernels: every K-step inside one filter tap (C4 % 64 == 0),
+    // or a 1x1 filter over 16-byte pixels whose last K-step runs into the
+    // next pixels (zero weights there)
+    const bool one_tap = d.R == 1 && d.S == 1 && C4 % 16 == 0;
+    const bool tap_ok = (C4 % 64 == 0 || one_tap) && d.R <= 16 && d.S <= 16;
     // row-pair mode of the LDS-direct kernel for small channel counts (the
     // 3-channel stems): two filter rows of S * C4 <= 32 bytes per K-step,
     // over a zero-point padded copy of the image
-    // (1x1 convolutions whose pixels are whole 16-byte chunks gather them
-    // directly: the padded copy would only cost a pass over x)
-    const bool whole_chunks_1x1 = d.R == 1 && d.S == 1 && C4 % 16 == 0;
     const bool rowpack = !tap_ok && C4 * d.S <= 32 && d.R <= 32 && d.cp.dil_h == 1 && d.cp.dil_w == 1 && !term3 &&
-                         !whole_chunks_1x1 && env_int("QNN_ROWPACK", 1) != 0 && env_int("QNN_TILE", -1) < 0;
+                         env_int("QNN_ROWPACK", 1) != 0 && env_int("QNN_TILE", -1) < 0;
     const int npairs = (d.R + 1) / 2;
     const int Jr = npairs * 64;                      // row-pair reduction length
     const int Hp = std::max(d.H + d.cp.pad_top + d.cp.pad_bottom, (Ho - 1) * d.cp.stride_h + 2 * npairs);
@@ -816,7 +826,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
                     cands.push_back({FAM_DMA, t});
         }
     } else {
-        cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok);
+        cands = conv_candidates(M, d.K, C4, (int)Jg, tap_ok, dma_ok, one_tap && C4 % 64 != 0);
     }
 
     const size_t wp_bytes = align_up((size_t)Kpad * Jpad, 256);

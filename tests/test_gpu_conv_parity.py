@@ -709,3 +709,42 @@ def test_window_channel_slice_output(coff):
     rest = np.ones(total, bool)
     rest[coff:coff + 72] = False
     assert (y[..., rest] == 77).all()
+
+
+# 1x1 convolutions whose channel count is a multiple of 16 but not of 64:
+# the tap-walk kernels run them with a last K-step that reads past each
+# pixel into the next ones (and past the end of x into out-of-range zeros),
+# against zero weights.  Forced LDS-direct (ring and short forms) and
+# register-staged tiles, plus the plan's own choice; stride 2, padding,
+# int8 input and output, weight zero points, int32 output.
+PARTIAL_1X1 = [
+    (W.ConvLayer("p16", 9, 10, 16, 40, 1, 1), 3, {}),
+    (W.ConvLayer("p48", 11, 9, 48, 72, 1, 1, 2), 2, dict(x_dtype="i8", yt="i8")),
+    (W.ConvLayer("p80", 8, 8, 80, 200, 1, 1, 1, (1, 0, 0, 1)), 2, dict(zp_w="channel")),
+    (W.ConvLayer("p144", 7, 9, 144, 24, 1, 1), 4, dict(yt="i32")),
+    (W.ConvLayer("p160", 13, 6, 160, 96, 1, 1), 2, dict(rounding="half_away")),
+    (W.ConvLayer("p208", 5, 5, 208, 130, 1, 1, 2, (1, 1, 1, 1)), 3, {}),
+]
+
+
+@pytest.mark.parametrize("forced", [{}, dict(QNN_DMA=0), dict(QNN_DMA=4), dict(QNN_DMA=12), dict(QNN_DMA=15),
+                                    dict(QNN_DMA=23), dict(QNN_DMA=24), dict(QNN_TAP=0), dict(QNN_TAP=3),
+                                    dict(QNN_TAP=7)],
+                         ids=["auto", "dma0", "dma4", "dma12", "short1", "short4a", "short4b", "tap0", "tap3", "tap7"])
+def test_one_by_one_partial_k_step(forced):
+    for i, (layer, N, kw) in enumerate(PARTIAL_1X1):
+        c = W.conv_case(layer, N, seed=900 + i, **kw)
+        with env(**forced):
+            p, keep = make_plan(c)
+            d = p.describe()
+            p.close()
+            if "QNN_DMA" in forced:
+                stages = DMA_SHORT_STAGES[forced["QNN_DMA"]]
+                if stages and -(-layer.Cin // 64) > stages:
+                    assert "cands=1 " not in d, d   # short form with fewer stages than K-steps: not forced
+                    continue
+                assert d.startswith("conv_dma"), d
+            if "QNN_TAP" in forced:
+                assert d.startswith("conv_tap"), d
+            log(f"partial 1x1 {forced} {layer.name}: {d}")
+            assert_equal(run_gpu(c), run_oracle(c), f"1x1 C={layer.Cin} {forced} {kw}: {d}")
