@@ -79,10 +79,12 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
 // taps outside the image) and term 3, then requantizes and stores, through
 // `stage` (LDS, at least TP * (TC + 16) bytes when a.staged) as whole
 // 16-byte pixel-row chunks, or directly.  Every wave must be past its last
-// read of `stage` before the call.
+// read of `stage` before the call.  `recs`, when given, holds the tile's
+// channel records (channels c0 .. c0 + TC - 1) in LDS, else they are read
+// from a.chan.
 template <int TC, int TP, int WC, int WP, int STAGE_BYTES>
 __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC / 16][TP / WP / 16], int8_t *stage,
-                                           int c0, int p0)
+                                           int c0, int p0, const ChanRec *recs = nullptr)
 {
     constexpr int NT = WC * WP * 64;
     constexpr int WTC = TC / WC, WTP = TP / WP;
@@ -132,7 +134,7 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
             v4i rec[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                rec[e] = *(const v4i *)(a.chan + c0 + cl + e);
+                rec[e] = *(const v4i *)(recs ? recs + cl + e : a.chan + c0 + cl + e);
 #pragma unroll
             for (int j = 0; j < FP; ++j) {
                 const int pl = wpos * WTP + j * 16 + lrow;
@@ -171,7 +173,7 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
         v4i rec[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            rec[e] = *(const v4i *)(a.chan + ch + e);
+            rec[e] = *(const v4i *)(recs ? recs + (ch - c0) + e : a.chan + ch + e);
 #pragma unroll
         for (int j = 0; j < FP; ++j) {
             const int m = mb + j * 16;

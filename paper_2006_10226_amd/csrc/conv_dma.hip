@@ -103,6 +103,8 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
     static_assert(SHORT || NS >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
 
     __shared__ __attribute__((aligned(1024))) int8_t lds[LDS_BYTES];
+    // the tile's channel records, fetched at the start for the epilogue
+    __shared__ __attribute__((aligned(16))) ChanRec recs[TC];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -123,6 +125,16 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0, a.N * a.H * a.W * a.C, kBufFlags);
     const __amdgpu_buffer_rsrc_t rw =
         __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, (short)0, a.Kpad * a.Jpad, kBufFlags);
+    if (wave == NW - 1) {
+        // records c0 .. c0 + TC - 1 (c0 + TC <= Kpad), a kilobyte per load;
+        // older than this wave's stage loads, so every stage wait covers them
+        const __amdgpu_buffer_rsrc_t rc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.chan, (short)0, a.Kpad * (int)sizeof(ChanRec), kBufFlags);
+#pragma unroll
+        for (int q = 0; q < TC / 64; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (__attribute__((address_space(3))) void *)(recs + q * 64), 16,
+                                                     (c0 + q * 64 + lane) * (int)sizeof(ChanRec), 0, 0, 0);
+    }
 
     // A 16-row x 64-byte block: lane L of the LDS-direct load that writes
     // it lands at byte 16 * L, i.e. row L / 4, physical chunk L % 4, and
@@ -271,7 +283,7 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         step(std::integral_constant<int, 3>{});
         static_assert(NS <= 4, "short form holds at most four K-steps");
         __syncthreads();
-        store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0);
+        store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0, recs);
     } else {
         // ---- pipeline -----------------------------------------------------
         // NS - 1 stages of loads in flight; the fragments of stage k + 1 are
@@ -300,7 +312,7 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
             mfma(fa[0], fb[0]);
         wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
         __syncthreads();
-        store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0);
+        store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0, recs);
     }
 }
 

@@ -59,6 +59,8 @@ __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>(
     static_assert(WTC % 16 == 0 && WTP % 16 == 0, "wave tile");
 
     __shared__ __attribute__((aligned(16))) int8_t lds[2 * STAGE];
+    // the tile's channel records, fetched at the start for the epilogue
+    __shared__ __attribute__((aligned(16))) ChanRec recs[TC];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -83,6 +85,15 @@ __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>(
         __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0, a.N * a.H * a.W * a.C, kBufFlags);
     const __amdgpu_buffer_rsrc_t rw =
         __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, (short)0, a.Kpad * a.Jpad, kBufFlags);
+    if (wave == WC * WP - 1) {
+        // records c0 .. c0 + TC - 1 (c0 + TC <= Kpad), a kilobyte per load
+        const __amdgpu_buffer_rsrc_t rc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.chan, (short)0, a.Kpad * (int)sizeof(ChanRec), kBufFlags);
+#pragma unroll
+        for (int q = 0; q < TC / 64; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (__attribute__((address_space(3))) void *)(recs + q * 64), 16,
+                                                     (c0 + q * 64 + lane) * (int)sizeof(ChanRec), 0, 0, 0);
+    }
 
     int voffA[A_PASS];
 #pragma unroll
@@ -232,7 +243,10 @@ __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>(
         __syncthreads();
     }
 
-    store_tile<TC, TP, WC, WP, 2 * STAGE>(a, acc, lds, c0, p0);
+    // the record loads (LDS-direct) have landed before anyone reads them
+    __builtin_amdgcn_s_waitcnt((0) | (7 << 4) | (15 << 8) | (0 << 14));
+    __syncthreads();
+    store_tile<TC, TP, WC, WP, 2 * STAGE>(a, acc, lds, c0, p0, recs);
 }
 
 // TapTile -> tile, K-step and wave grid.
