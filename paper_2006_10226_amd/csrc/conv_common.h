@@ -72,6 +72,26 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
     return packed;
 }
 
+// Adds bconst (bias and terms 2 and 4) of each block's four channels to the
+// accumulators of a WC x WP wave grid, from the tile's records in LDS (the
+// epilogue then leaves bconst out of the requantize).
+template <int TC, int TP, int WC, int WP>
+__device__ __forceinline__ void add_bconst(v4i (&acc)[TC / WC / 16][TP / WP / 16], const ChanRec *recs)
+{
+    constexpr int WTC = TC / WC, FC = WTC / 16, FP = TP / WP / 16;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wc = wave / WP;
+#pragma unroll
+    for (int i = 0; i < FC; ++i) {
+        const int cl = wc * WTC + i * 16 + (lane >> 4) * 4;
+        const v4i b = v4i{recs[cl].bconst, recs[cl + 1].bconst, recs[cl + 2].bconst, recs[cl + 3].bconst};
+#pragma unroll
+        for (int j = 0; j < FP; ++j)
+            acc[i][j] += b;
+    }
+}
+
 // Epilogue of one TC x TP tile held by NT/64 waves in a WC x WP grid of
 // (TC/WC) x (TP/WP) wave tiles of 16x16 MFMA blocks: lane holds channels
 // ch..ch+3 (4 * (lane >> 4) inside a 16-block) of pixel lane & 15 inside a
@@ -81,7 +101,8 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
 // 16-byte pixel-row chunks, or directly.  Every wave must be past its last
 // read of `stage` before the call.  `recs`, when given, holds the tile's
 // channel records (channels c0 .. c0 + TC - 1) in LDS, else they are read
-// from a.chan.
+// from a.chan; with `recs` the accumulators already hold bconst (see
+// add_bconst).
 template <int TC, int TP, int WC, int WP, int STAGE_BYTES>
 __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC / 16][TP / WP / 16], int8_t *stage,
                                            int c0, int p0, const ChanRec *recs = nullptr)
@@ -134,7 +155,11 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
             v4i rec[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
+            {
                 rec[e] = *(const v4i *)(recs ? recs + cl + e : a.chan + c0 + cl + e);
+                if (recs)
+                    rec[e].y = 0;
+            }
 #pragma unroll
             for (int j = 0; j < FP; ++j) {
                 const int pl = wpos * WTP + j * 16 + lrow;
@@ -173,7 +198,11 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
         v4i rec[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
+        {
             rec[e] = *(const v4i *)(recs ? recs + (ch - c0) + e : a.chan + ch + e);
+            if (recs)
+                rec[e].y = 0;
+        }
 #pragma unroll
         for (int j = 0; j < FP; ++j) {
             const int m = mb + j * 16;

@@ -271,6 +271,8 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
             constexpr int k = decltype(S)::value;
             if constexpr (k < NS) {
                 stage_barrier<LPS *(NS - 1 - k)>();
+                if constexpr (k == 0)
+                    add_bconst<TC, TP, WC, WP>(acc, recs);   // the records landed with stage 0
                 if (k < nk) {
                     read_frags(k, fa[0], fb[0]);
                     mfma(fa[0], fb[0]);
@@ -296,6 +298,7 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         for (int s = 0; s < NS - 1; ++s)
             issue(s);
         stage_barrier<LPS *(NS - 2)>();
+        add_bconst<TC, TP, WC, WP>(acc, recs);   // the records landed with stage 0
         read_frags(0, fa[0], fb[0]);
         int k = 0;
         for (; k + 2 <= nk; k += 2) {

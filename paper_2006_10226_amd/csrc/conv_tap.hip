@@ -226,7 +226,10 @@ __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>(
     load(RA0, RB0, X0, 0);
     load(RA1, RB1, X1, 1);
     store(0, RA0, RB0, X0);
+    // the record loads are older than stage 0's, whose data store() waited
+    // for; the barrier publishes them
     __syncthreads();
+    add_bconst<TC, TP, WC, WP>(acc, recs);
     int k = 0;
     for (; k + 2 <= nk; k += 2) {
         load(RA0, RB0, X0, k + 2);
