@@ -78,6 +78,8 @@ __global__ void __launch_bounds__(wave_count<KSPLIT>() * 64, (KSPLIT > 4 ? 1 : 2
     // LDS: four wave rings; reused for the partial sums (4 x 16 KB) and the
     // output staging (TPW tiles of 64 pixels x 80 bytes)
     __shared__ __attribute__((aligned(1024))) int8_t lds[NWV * RING];
+    // channel records of each tile of the workgroup, fetched at the start
+    __shared__ __attribute__((aligned(16))) ChanRec wrec[TPW][64];
     static_assert(RING >= 64 * 64 * 4, "partial sums must fit");
 
     const int tid = threadIdx.x;
@@ -194,12 +196,28 @@ __global__ void __launch_bounds__(wave_count<KSPLIT>() * 64, (KSPLIT > 4 ? 1 : 2
     // operand fragments of the activations: lane row lrow, chunk lchk
     const int lrow = lane & 15, lchk = lane >> 4;
     const int co = lrow * BK + ((lchk ^ sw64w(lrow)) << 4);
+    // the first wave of each tile fetches the tile's 64 channel records into
+    // LDS (the epilogue reads them after the loop's final barrier), and
+    // starts its sums at bconst; the other waves of a split start at 0
+    if (ks_id == 0) {
+        const __amdgpu_buffer_rsrc_t rc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.chan, (short)0, a.Kpad * (int)sizeof(ChanRec), kBufFlags);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (__attribute__((address_space(3))) void *)wrec[tl], 16,
+                                                 (c0 + lane) * (int)sizeof(ChanRec), 0, 0, 0);
+    }
     v4i acc[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
+        v4i b0 = v4i{0, 0, 0, 0};
+        if (ks_id == 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                b0[e] = a.chan[c0 + i * 16 + lchk * 4 + e].bconst;
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            acc[i][j] = v4i{0, 0, 0, 0};
+            acc[i][j] = b0;
+    }
     auto step = [&](int n, v4i (&A)[4]) {
         const int8_t *src = ring + (n & (NS - 1)) * BSTAGE + co;
         v4i fb[4];
@@ -302,7 +320,10 @@ __global__ void __launch_bounds__(wave_count<KSPLIT>() * 64, (KSPLIT > 4 ? 1 : 2
         v4i rec[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            rec[e] = *(const v4i *)(a.chan + ch + e);
+        {
+            rec[e] = *(const v4i *)(wrec[tl] + (ch - c0) + e);
+            rec[e].y = 0;   // bconst is in the sums already
+        }
         if (staged) {
             *(uint32_t *)(stage + (j * 16 + lrow) * SP + i * 16 + lchk * 4) = requant4(a, v, rec);
             continue;
