@@ -357,8 +357,26 @@ def main():
     roof["avg_launch_us_event_bracketed"] = round(D["ms"] / D["launches"] * 1e3, 3)
     roof["launches_per_step"] = D["launches"]
 
-    roof_us = sum(max(2.0 * it.macs / (PEAK_INT8_TOPS * 1e12), it.bytes / (PEAK_HBM_GBS * 1e9)) * 1e6
-                  for it in items)
+    def roofline_us(it):
+        return max(2.0 * it.macs / (PEAK_INT8_TOPS * 1e12), it.bytes / (PEAK_HBM_GBS * 1e9)) * 1e6
+
+    roof_us = sum(roofline_us(it) for it in items)
+    # Layers whose own roofline lets them reach at least 70% of the MFMA
+    # peak (ops per byte at or above 0.7 x the ridge: the 3x3 convs and the
+    # 1x1 convs with many input channels), aggregated over their share of
+    # the step; the whole stack's ceiling beside it.
+    cb = [(it, float(t) * scale) for it, t in zip(items, per)
+          if it.macs and 2.0 * it.macs / max(it.bytes, 1) >= 0.7 * ridge]
+    compute_bound = None
+    if cb:
+        cb_ops = sum(2.0 * it.macs for it, _ in cb)
+        cb_ms = sum(t for _, t in cb)
+        cb_roof_us = sum(roofline_us(it) for it, _ in cb)
+        cb_tops = cb_ops / (cb_ms * 1e-3) / 1e12
+        compute_bound = {"layers": len(cb), "tops": round(cb_tops, 1),
+                         "frac_of_int8_peak": round(cb_tops / PEAK_INT8_TOPS, 4),
+                         "ceiling_frac_of_int8_peak": round(cb_ops / (cb_roof_us * 1e-6) / 1e12 / PEAK_INT8_TOPS, 4),
+                         "share_of_step": round(cb_ms / ms, 4)}
     layer_rows = []
     for it, t in zip(items, per):
         row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3),
@@ -366,7 +384,10 @@ def main():
         if it.macs:
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
         row["gbs"] = round(it.bytes / (float(t) * 1e-3) / 1e9, 1)
-        row["roofline_us"] = round(max(2.0 * it.macs / (PEAK_INT8_TOPS * 1e12), it.bytes / (PEAK_HBM_GBS * 1e9)) * 1e6, 3)
+        row["roofline_us"] = round(roofline_us(it), 3)
+        row["frac_of_roofline"] = round(roofline_us(it) / (float(t) * 1e3), 4)
+        if it.macs:
+            row["frac_of_int8_peak"] = round(row["tops"] / PEAK_INT8_TOPS, 4)
         layer_rows.append(row)
     if args.layers_out:
         os.makedirs(os.path.dirname(os.path.abspath(args.layers_out)), exist_ok=True)
@@ -400,7 +421,11 @@ def main():
                    "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4),
                    # sum over layers of max(MFMA time at peak, algorithmic bytes at HBM peak),
                    # over the measured step: the whole stack's fraction of its roofline
-                   "stack_roofline_frac": round(roof_us / (ms * 1e3), 4)},
+                   "stack_roofline_frac": round(roof_us / (ms * 1e3), 4),
+                   # the best the stack could reach: every layer at its own roofline
+                   "stack_ceiling_frac_of_int8_peak": round(2.0 * total_macs / (roof_us * 1e-6) / 1e12
+                                                            / PEAK_INT8_TOPS, 4),
+                   "compute_bound_layers": compute_bound},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -58,7 +58,7 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
         for (int e = 0; e < 4; ++e) {
             const int v = (int)((uint32_t)acc[e] + (uint32_t)rec[e].y);
             const int t = (__mulhi(v, rec[e].x) + rec[e].z) >> (rec[e].w & 31);   // shift - 32: shift is in [33, 53]
-            packed |= (uint32_t)min(max(t, a.lo_off), a.hi_off) << (8 * e);
+            packed |= (uint32_t)clamp_i32(t, a.lo_off, a.hi_off) << (8 * e);
         }
         return packed ^ a.out_xor;
     }
@@ -72,23 +72,75 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
     return packed;
 }
 
+// 16-byte LDS read issued as inline assembly.  The compiler orders every LDS
+// read it sees after all LDS-direct loads still in flight (it cannot tell
+// which LDS bytes they write), which drains a ring of staged K-steps at
+// every step; the kernels that read a ring this way order each read after
+// the loads of its own stage themselves (vmcnt waits and barriers).  The
+// result may be used only after lds_settle.
+__device__ __forceinline__ v4i lds_read16(const int8_t *p)
+{
+    v4i r;
+    const uint32_t addr = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) int8_t *)p;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+    return r;
+}
+
+// Waits until at most N of this wave's LDS reads (the N issued last) are in
+// flight, then marks the given fragments as produced after the wait, so
+// that no use of them is scheduled before it.
+template <int N>
+__device__ __forceinline__ void lds_wait()
+{
+    static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+template <int F>
+__device__ __forceinline__ void lds_settled(v4i (&f)[F])
+{
+#pragma unroll
+    for (int i = 0; i < F; ++i)
+        asm volatile("" : "+v"(f[i]));
+}
+
 // Adds bconst (bias and terms 2 and 4) of each block's four channels to the
 // accumulators of a WC x WP wave grid, from the tile's records in LDS (the
-// epilogue then leaves bconst out of the requantize).
-template <int TC, int TP, int WC, int WP>
+// epilogue then leaves bconst out of the requantize).  ASYNC: the records
+// are read with lds_read16 (the caller's waits cover their LDS-direct load).
+template <int TC, int TP, int WC, int WP, bool ASYNC = false>
 __device__ __forceinline__ void add_bconst(v4i (&acc)[TC / WC / 16][TP / WP / 16], const ChanRec *recs)
 {
     constexpr int WTC = TC / WC, FC = WTC / 16, FP = TP / WP / 16;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wc = wave / WP;
+    if constexpr (ASYNC) {
+        v4i r[FC * 4];
 #pragma unroll
-    for (int i = 0; i < FC; ++i) {
-        const int cl = wc * WTC + i * 16 + (lane >> 4) * 4;
-        const v4i b = v4i{recs[cl].bconst, recs[cl + 1].bconst, recs[cl + 2].bconst, recs[cl + 3].bconst};
+        for (int i = 0; i < FC; ++i) {
+            const int cl = wc * WTC + i * 16 + (lane >> 4) * 4;
 #pragma unroll
-        for (int j = 0; j < FP; ++j)
-            acc[i][j] += b;
+            for (int e = 0; e < 4; ++e)
+                r[i * 4 + e] = lds_read16((const int8_t *)(recs + cl + e));
+        }
+        lds_wait<0>();
+        lds_settled(r);
+#pragma unroll
+        for (int i = 0; i < FC; ++i) {
+            const v4i b = v4i{r[i * 4][1], r[i * 4 + 1][1], r[i * 4 + 2][1], r[i * 4 + 3][1]};
+#pragma unroll
+            for (int j = 0; j < FP; ++j)
+                acc[i][j] += b;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < FC; ++i) {
+            const int cl = wc * WTC + i * 16 + (lane >> 4) * 4;
+            const v4i b = v4i{recs[cl].bconst, recs[cl + 1].bconst, recs[cl + 2].bconst, recs[cl + 3].bconst};
+#pragma unroll
+            for (int j = 0; j < FP; ++j)
+                acc[i][j] += b;
+        }
     }
 }
 

@@ -237,17 +237,26 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         for (int j = 0; j < FP; ++j)
             acc[i][j] = v4i{0, 0, 0, 0};
     v4i fa[2][FC], fb[2][FP];
+    // fragment reads as lds_read16: the stage waits and barriers below order
+    // them after their stage's LDS-direct loads, while the compiler would
+    // wait for every stage in flight
+    static_assert(FC + FP <= 15, "fragment reads of one step exceed the lgkmcnt range");
     auto read_frags = [&](int ks, v4i (&A)[FC], v4i (&B)[FP]) {
         const int8_t *As = lds + (ks & (NS - 1)) * STAGE + (wc * WTC + lrow) * BK + co;
         const int8_t *Bs = lds + (ks & (NS - 1)) * STAGE + TC * BK + (wpos * WTP + lrow) * BK + co;
 #pragma unroll
         for (int i = 0; i < FC; ++i)
-            A[i] = *(const v4i *)(As + i * 16 * BK);
+            A[i] = lds_read16(As + i * 16 * BK);
 #pragma unroll
         for (int j = 0; j < FP; ++j)
-            B[j] = *(const v4i *)(Bs + j * 16 * BK);
+            B[j] = lds_read16(Bs + j * 16 * BK);
     };
-    auto mfma = [&](const v4i (&A)[FC], v4i (&B)[FP]) {
+    // MFMAs of one step; NEWER: fragment reads issued after A and B's, which
+    // may stay in flight
+    auto mfma = [&](auto NEWER, v4i (&A)[FC], v4i (&B)[FP]) {
+        lds_wait<decltype(NEWER)::value>();
+        lds_settled(A);
+        lds_settled(B);
         if constexpr (FLIP) {
 #pragma unroll
             for (int j = 0; j < FP; ++j)
@@ -272,10 +281,10 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
             if constexpr (k < NS) {
                 stage_barrier<LPS *(NS - 1 - k)>();
                 if constexpr (k == 0)
-                    add_bconst<TC, TP, WC, WP>(acc, recs);   // the records landed with stage 0
+                    add_bconst<TC, TP, WC, WP, true>(acc, recs);   // the records landed with stage 0
                 if (k < nk) {
                     read_frags(k, fa[0], fb[0]);
-                    mfma(fa[0], fb[0]);
+                    mfma(std::integral_constant<int, 0>{}, fa[0], fb[0]);
                 }
             }
         };
@@ -298,21 +307,22 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         for (int s = 0; s < NS - 1; ++s)
             issue(s);
         stage_barrier<LPS *(NS - 2)>();
-        add_bconst<TC, TP, WC, WP>(acc, recs);   // the records landed with stage 0
+        add_bconst<TC, TP, WC, WP, true>(acc, recs);   // the records landed with stage 0
         read_frags(0, fa[0], fb[0]);
+        constexpr std::integral_constant<int, FC + FP> kNext{};
         int k = 0;
         for (; k + 2 <= nk; k += 2) {
             stage_barrier<LPS *(NS - 3)>();
             issue(k + NS - 1);
             read_frags(k + 1, fa[1], fb[1]);
-            mfma(fa[0], fb[0]);
+            mfma(kNext, fa[0], fb[0]);
             stage_barrier<LPS *(NS - 3)>();
             issue(k + NS);
             read_frags(k + 2, fa[0], fb[0]);
-            mfma(fa[1], fb[1]);
+            mfma(kNext, fa[1], fb[1]);
         }
         if (k < nk)
-            mfma(fa[0], fb[0]);
+            mfma(std::integral_constant<int, 0>{}, fa[0], fb[0]);
         wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
         __syncthreads();
         store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0, recs);

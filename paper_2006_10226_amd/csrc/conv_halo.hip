@@ -55,10 +55,12 @@ struct HaloGeom {
     int nst;      // K-steps of the filter: R * S * C / 64
     int jsteps;   // K-steps per 16-row block of the operand-order weights: Jpad / 64
     int nwg_p;    // workgroups per 64-channel tile: N * gpi
+    int sep;      // 1: the staging tiles have LDS of their own (no barrier before the epilogue)
 };
 
 constexpr int kHaloR = 3, kHaloS = 3;
 constexpr int kStagePitch = 80;   // staging row: 64 output bytes + pad
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 bool halo_geometry(const ConvArgs &a, int nw, HaloGeom *g)
 {
@@ -86,6 +88,11 @@ bool halo_geometry(const ConvArgs &a, int nw, HaloGeom *g)
     if (nwg_p * ((a.K + 63) / 64) >= (1LL << 31))
         return false;
     g->nwg_p = (int)nwg_p;
+    // separate staging space when it keeps the occupancy the launch bounds
+    // ask for (one 8-wave or two 4-wave workgroups per CU)
+    const size_t stage = (size_t)nw * 64 * kStagePitch;
+    const size_t base = (size_t)g->nst * 4096 + 1024 + (size_t)g->wbytes;
+    g->sep = base + stage <= (nw == 8 ? kLdsPerCu : kLdsPerCu / 2) ? 1 : 0;
     return true;
 }
 
@@ -119,30 +126,12 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
         __builtin_amdgcn_make_buffer_rsrc((void *)a.wf, (short)0, a.Kpad * a.Jpad, kBufFlags);
 
     // LDS: weights [4][nst] fragments of 1 KB, the 64 channel records, the
-    // window; after the main loop the window's space holds one staging tile
-    // per wave
+    // window, then one staging tile per wave (g.sep), else the staging tiles
+    // reuse the window's space after the main loop
     int8_t *wts = smem;
     int8_t *recs = smem + g.nst * 4096;
     int8_t *win = recs + 1024;
-    int8_t *stage = win + wave * (64 * kStagePitch);
-
-    // weights in MFMA operand order: fragment (16-row block b, step s) of the
-    // packed copy is the kilobyte at (b * jsteps + s) * 1024; LDS fragment
-    // f = i * nst + st holds block c0 / 16 + i, step st
-    for (int f = wave; f < 4 * g.nst; f += NW) {
-        const int i = f / g.nst;
-        const int st = f - i * g.nst;
-        const int src = ((c0 / 16 + i) * g.jsteps + st) * 1024;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wts + f * 1024), 16,
-                                                 lane * 16, src, 0, 0);
-    }
-
-    if (wave == NW - 1) {
-        const __amdgpu_buffer_rsrc_t rc =
-            __builtin_amdgcn_make_buffer_rsrc((void *)a.chan, (short)0, a.Kpad * (int)sizeof(ChanRec), kBufFlags);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (__attribute__((address_space(3))) void *)recs, 16,
-                                                 (c0 + lane) * (int)sizeof(ChanRec), 0, 0, 0);
-    }
+    int8_t *stage = win + (g.sep ? g.wbytes : 0) + wave * (64 * kStagePitch);
 
     uint32_t oob = 0;   // bit u: this lane's cell of the wave's load u is outside the image
     // window: load k (of every slice cc) fills cells 16 k .. 16 k + 15 and is
@@ -166,6 +155,25 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
                     0, 0);
         }
     }
+    // weights, after the window (its loads go to HBM, these mostly hit the
+    // L2), in MFMA operand order: fragment (16-row block b, step s) of the
+    // packed copy is the kilobyte at (b * jsteps + s) * 1024; LDS fragment
+    // f = i * nst + st holds block c0 / 16 + i, step st
+    for (int f = wave; f < 4 * g.nst; f += NW) {
+        const int i = f / g.nst;
+        const int st = f - i * g.nst;
+        const int src = ((c0 / 16 + i) * g.jsteps + st) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wts + f * 1024), 16,
+                                                 lane * 16, src, 0, 0);
+    }
+
+    if (wave == NW - 1) {
+        const __amdgpu_buffer_rsrc_t rc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)a.chan, (short)0, a.Kpad * (int)sizeof(ChanRec), kBufFlags);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (__attribute__((address_space(3))) void *)recs, 16,
+                                                 (c0 + lane) * (int)sizeof(ChanRec), 0, 0, 0);
+    }
+
     wait_vm<0>();
 
     // the window as x': padding cells hold zp_x', image cells are legalised.
@@ -257,21 +265,26 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
         for (int t = 0; t < kHaloR * kHaloS; ++t) {
             if (t + 1 < kHaloR * kHaloS)
                 load_tap(hl, cc, t + 1, A[(t + 1) & 1], B[(t + 1) & 1]);
+            // keep the order: the reads of tap t + 1 are issued before the
+            // MFMAs of tap t (the scheduler otherwise moves each read next
+            // to its first use and waits on it there)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[t & 1][i], B[t & 1][j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
     // ---- epilogue ------------------------------------------------------------
     // block (i, j): channels c0 + 16 i + 4 lchk .. +3 of pixel m0 + 16 j + lrow.
-    // The staging tiles overwrite the window once every wave is past its
-    // reads of it; a staging tile is one wave's own (LDS accesses of one
-    // wave run in order).
+    // Staging tiles in the window's space overwrite it once every wave is
+    // past its reads of it; a staging tile is one wave's own (LDS accesses
+    // of one wave run in order).
     const bool staged = a.staged && a.mode == OUT_REQUANT;
-    if (staged)
+    if (staged && !g.sep)
         __syncthreads();
     v4i zw[4];
     if (a.asum) {
@@ -356,7 +369,16 @@ size_t halo_lds_bytes(const ConvArgs &a, int nw)
     if (!halo_geometry(a, nw, &g))
         return 0;
     const size_t stage = (size_t)nw * 64 * kStagePitch;
-    return (size_t)g.nst * 4096 + 1024 + ((size_t)g.wbytes > stage ? (size_t)g.wbytes : stage);
+    const size_t base = (size_t)g.nst * 4096 + 1024;
+    return g.sep ? base + g.wbytes + stage : base + ((size_t)g.wbytes > stage ? (size_t)g.wbytes : stage);
+}
+
+int halo_layout(const ConvArgs &a, int nw)
+{
+    HaloGeom g;
+    if (!halo_geometry(a, nw, &g))
+        return -1;
+    return g.sep;
 }
 
 long long halo_pixel_tiles(const ConvArgs &a)

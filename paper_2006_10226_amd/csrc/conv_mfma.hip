@@ -371,7 +371,7 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
                     for (int e = 0; e < 4; ++e) {
                         const int hi = __mulhi(vals[e], mult[e]);
                         const int t = (hi + rndzp[e]) >> (shift[e] & 31);   // shift - 32 for shift in [33, 53]
-                        u[e] = (uint32_t)min(max(t, a.lo_off), a.hi_off);
+                        u[e] = (uint32_t)clamp_i32(t, a.lo_off, a.hi_off);
                     }
                     packed = (u[0] | (u[1] << 8) | (u[2] << 16) | (u[3] << 24)) ^ a.out_xor;
                 } else {
@@ -438,7 +438,7 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
                     for (int e = 0; e < 4; ++e) {
                         const int v = (int)((uint32_t)acc[i][jj][e] + (uint32_t)bconst[e]);
                         const int t = (__mulhi(v, mult[e]) + rndzp[e]) >> (shift[e] & 31);   // shift - 32 for shift in [33, 53]
-                        u[e] = (uint32_t)min(max(t, a.lo_off), a.hi_off);
+                        u[e] = (uint32_t)clamp_i32(t, a.lo_off, a.hi_off);
                     }
                     packed = (u[0] | (u[1] << 8) | (u[2] << 16) | (u[3] << 24)) ^ a.out_xor;
                 } else {

@@ -220,11 +220,17 @@ __global__ void __launch_bounds__(wave_count<KSPLIT>() * 64, (KSPLIT > 4 ? 1 : 2
     }
     auto step = [&](int n, v4i (&A)[4]) {
         const int8_t *src = ring + (n & (NS - 1)) * BSTAGE + co;
+        // lds_read16: the wait for stage n above orders these reads after its
+        // LDS-direct loads; the compiler would wait for every stage in flight
         v4i fb[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            fb[j] = *(const v4i *)(src + j * 16 * BK);
-            if constexpr (FLIP)
+        for (int j = 0; j < 4; ++j)
+            fb[j] = lds_read16(src + j * 16 * BK);
+        lds_wait<0>();
+        lds_settled(fb);
+        if constexpr (FLIP) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
                 fb[j] ^= v4i{(int)0x80808080, (int)0x80808080, (int)0x80808080, (int)0x80808080};
         }
 #pragma unroll

@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(256) depthwise3_kernel(DwArgs a)
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 const int t = (__mulhi(v[c], cr[c].mult) + cr[c].rndzp) >> (cr[c].shift & 31);   // shift - 32
-                packed[c >> 2] |= (uint32_t)min(max(t, a.lo_off), a.hi_off) << (8 * (c & 3));
+                packed[c >> 2] |= (uint32_t)clamp_i32(t, a.lo_off, a.hi_off) << (8 * (c & 3));
             }
             packed[0] ^= a.out_xor;
             packed[1] ^= a.out_xor;

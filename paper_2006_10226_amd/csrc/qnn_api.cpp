@@ -1028,6 +1028,10 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     } else if (best.fam == FAM_WIN) {
         const size_t n = strlen(buf);
         snprintf(buf + n, sizeof buf - n, " cfg=%d", best.tile);
+    } else if (best.fam == FAM_HALO) {
+        const int lay = halo_layout(a, best.tile);
+        const size_t n = strlen(buf);
+        snprintf(buf + n, sizeof buf - n, " sep=%d", lay);
     }
     p->desc = buf;
     *out = p;

@@ -24,6 +24,15 @@ struct ChanRec {
 
 enum OutMode { OUT_REQUANT = 0, OUT_INT32 = 1 };
 
+// min(max(t, lo), hi) for lo <= hi (the host rejects empty clamps) in one
+// VALU operation; the compiler emits a max and a min for runtime bounds.
+__device__ __forceinline__ int clamp_i32(int t, int lo, int hi)
+{
+    int r;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(t), "v"(lo), "v"(hi));
+    return r;
+}
+
 // Implicit-GEMM conv arguments.  GEMM view: D[k][m] = sum_j Wp[k][j] * X'[m][j]
 // with m = output pixel, k = output channel, j = (r*S + s)*C + c.
 struct ConvArgs {
@@ -197,6 +206,9 @@ int wave_threads(int split);
 // per 64-channel tile, -1 when not eligible.
 size_t halo_lds_bytes(const ConvArgs &a, int nw);
 long long halo_pixel_tiles(const ConvArgs &a);
+// 1: the staging tiles have LDS of their own, 0: they reuse the window's
+// (-1: not eligible)
+int halo_layout(const ConvArgs &a, int nw);
 hipError_t launch_conv_halo(const ConvArgs &a, int nw, hipStream_t st);
 // Streaming window kernel (conv_window.hip): stride 1, undilated 3x3,
 // C % 64 == 0, Wo <= 64; the input window of a workgroup's bands stays in

@@ -590,6 +590,7 @@ def _halo_lds(layer, nw):
 @pytest.mark.parametrize("nw", [4, 8])
 def test_every_halo_config(nw):
     ran = 0
+    seps = set()
     for i, (layer, N, kw) in enumerate(HALO_SHAPES):
         c = W.conv_case(layer, N, seed=700 + nw * 10 + i, **kw)
         with env(QNN_HALO=nw):
@@ -600,10 +601,13 @@ def test_every_halo_config(nw):
                 assert _halo_lds(layer, nw) > 160 * 1024, d
                 continue
             assert f"threads={nw * 64}" in d, d
+            seps.add(d.split("sep=")[1].split()[0])
             log(f"halo nw {nw} shape {layer.name}: {d}")
             assert_equal(run_gpu(c), run_oracle(c), f"halo nw {nw} {layer.name} {kw}")
             ran += 1
     assert ran >= 5
+    # both staging layouts: tiles in LDS of their own, tiles over the window
+    assert seps == {"0", "1"}, seps
     # zero point 0: no padding correction table
     c = W.conv_case(HALO_SHAPES[2][0], 2, seed=9)
     c.zp_x = 0
