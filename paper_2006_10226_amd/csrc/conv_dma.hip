@@ -323,6 +323,10 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         }
         if (k < nk)
             mfma(std::integral_constant<int, 0>{}, fa[0], fb[0]);
+        // with an even step count the reads of step nk (past the last one)
+        // are still in flight: retire them before their registers are
+        // reused (the compiler does not know they are pending)
+        lds_wait<0>();
         wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
         __syncthreads();
         store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0, recs);

@@ -14,8 +14,9 @@
 // input byte once per filter tap (nine times for 3x3) and every weight once
 // per tile through the vector memory path.  Here a wave fetches its window
 // of (NW * TR + 2) x (Wo + 2) pixels once (LDS-direct buffer loads, the
-// waves taking turns), then rewrites it in place as x': cells outside the image become zp_x', the
-// others are legalised (XOR 0x80 for uint8) once instead of at every read.
+// waves taking turns) and fills the cells outside the image with zp_x'
+// (held as zp_x' XOR 0x80 for uint8, because every fragment is legalised
+// with one XOR after it is read; the XORs issue beside the MFMAs).
 // The nine taps are nine shifted LDS views of the window: for output pixel
 // (t, w) of the tile and tap (r, s) the operand row is window cell
 // (t + r, w + s).  The accumulators start at the per-channel constant
@@ -176,32 +177,19 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
 
     wait_vm<0>();
 
-    // the window as x': padding cells hold zp_x', image cells are legalised.
-    // Each lane rewrites the 16 bytes it loaded (LDS accesses of one wave
-    // run in order); the barrier below publishes the result to all waves.
+    // padding cells: each lane overwrites the 16 bytes of its loads that fell
+    // outside the image (LDS accesses of one wave run in order; the barrier
+    // below publishes them) with zp_x' in the stored form of the window,
+    // which is x' XOR 0x80 for uint8 (the fragments are legalised with one
+    // XOR after they are read)
     {
-        const v4i zp = v4i{(int)a.zp4, (int)a.zp4, (int)a.zp4, (int)a.zp4};
-        const v4i fl = v4i{(int)0x80808080, (int)0x80808080, (int)0x80808080, (int)0x80808080};
+        const int zs = (int)(a.zp4 ^ (FLIP ? 0x80808080u : 0u));
+        const v4i zp = v4i{zs, zs, zs, zs};
         for (int cc = 0; cc < cch; ++cc) {
             int8_t *base = win + (cc * g.ninst + wave) * 1024 + lane * 16;
-            // four loads at a time: their reads are in flight together
-            for (int u0 = 0; u0 < nmine; u0 += 4) {
-                v4i v[4];
-#pragma unroll
-                for (int d = 0; d < 4; ++d)
-                    if (FLIP && u0 + d < nmine && !((oob >> (u0 + d)) & 1u))
-                        v[d] = *(const v4i *)(base + (u0 + d) * NW * 1024);
-#pragma unroll
-                for (int d = 0; d < 4; ++d) {
-                    if (u0 + d >= nmine)
-                        continue;
-                    const bool out = (oob >> (u0 + d)) & 1u;
-                    if (out)
-                        *(v4i *)(base + (u0 + d) * NW * 1024) = zp;
-                    else if (FLIP)
-                        *(v4i *)(base + (u0 + d) * NW * 1024) = v[d] ^ fl;
-                }
-            }
+            for (int u = 0; u < nmine; ++u)
+                if ((oob >> u) & 1u)
+                    *(v4i *)(base + u * NW * 1024) = zp;
         }
     }
     __syncthreads();   // every wave's share of the weights and records has landed
@@ -257,6 +245,13 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
             B[j] = *(const v4i *)(hl + q * 64 + ((lchk ^ cell_swz(q)) << 4));
         }
     };
+    auto legalise = [&](v4i (&B)[4]) __attribute__((always_inline)) {
+        if constexpr (FLIP) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                B[j] ^= v4i{(int)0x80808080, (int)0x80808080, (int)0x80808080, (int)0x80808080};
+        }
+    };
     for (int cc = 0; cc < cch; ++cc) {
         const int8_t *hl = win + cc * g.ninst * 1024;
         v4i A[2][4], B[2][4];
@@ -269,6 +264,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
             // MFMAs of tap t (the scheduler otherwise moves each read next
             // to its first use and waits on it there)
             __builtin_amdgcn_sched_barrier(0);
+            legalise(B[t & 1]);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
