@@ -85,10 +85,16 @@ constexpr int dma_occupancy()
 // channels).  All NS stages are issued at once into their own buffers (no
 // ring), so the LDS footprint is only NS stages and more workgroups stay
 // resident to cover the memory latency of these one-pass tiles.
-template <int TC, int TP, int WC, int WP, int NS, bool FLIP, bool SHORT>
-__global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>())) conv_dma_kernel(ConvArgs a)
+// KS = 2 (ring form only): two groups of WC x WP waves share the tile and
+// take alternate K-steps, each through its own half of the ring (NS / 2
+// stages); the second group's partial sums are added through LDS before
+// the first group's epilogue.  For tiles too few to fill the chip this
+// puts two waves on each SIMD and twice the MFMA work behind each barrier.
+template <int TC, int TP, int WC, int WP, int NS, bool FLIP, bool SHORT, int KS = 1>
+__global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<TC / WC, TP / WP>()))
+    conv_dma_kernel(ConvArgs a)
 {
-    constexpr int NW = WC * WP;
+    constexpr int NW = WC * WP;     // waves of one group
     constexpr int BK = 64;
     constexpr int WTC = TC / WC, WTP = TP / WP;
     constexpr int FC = WTC / 16, FP = WTP / 16;
@@ -96,11 +102,14 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
     constexpr int LA = TC / (16 * NW);   // 1 KB weight blocks per wave per stage
     constexpr int LB = TP / (16 * NW);   // 1 KB activation blocks per wave per stage
     constexpr int LPS = LA + LB;         // loads per lane per stage
+    constexpr int NSG = NS / KS;        // ring stages of one group
     constexpr int LDS_BYTES = NS * STAGE > TP * (TC + 16) ? NS * STAGE : TP * (TC + 16);
     static_assert(TC % (16 * NW) == 0 && TP % (16 * NW) == 0, "every wave loads whole 16-row blocks");
-    static_assert((NS & (NS - 1)) == 0, "stage count is a power of two");
-    static_assert(LPS * (SHORT ? NS - 1 : NS - 2) < 64, "vmcnt range");
-    static_assert(SHORT || NS >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
+    static_assert((NS & (NS - 1)) == 0 && (NSG & (NSG - 1)) == 0, "stage counts are powers of two");
+    static_assert(KS == 1 || KS == 2, "one or two K-step groups");
+    static_assert(KS == 1 || (!SHORT && NW * FC * FP * 1024 <= LDS_BYTES), "split groups: ring form, partials fit");
+    static_assert(LPS * (SHORT ? NS - 1 : NSG - 2) < 64, "vmcnt range");
+    static_assert(SHORT || NSG >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
 
     __shared__ __attribute__((aligned(1024))) int8_t lds[LDS_BYTES];
     // the tile's channel records, fetched at the start for the epilogue
@@ -108,7 +117,9 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
+    const int wave_id = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
+    const int grp = wave_id / NW;     // K-step group: steps grp, grp + KS, ...
+    const int wave = wave_id % NW;    // wave inside its group
     const int wc = wave / WP, wpos = wave % WP;
 
     // XCD x (workgroups dealt round-robin) takes the x-th eighth of the
@@ -125,7 +136,7 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         __builtin_amdgcn_make_buffer_rsrc((void *)a.x, (short)0, a.N * a.H * a.W * a.C, kBufFlags);
     const __amdgpu_buffer_rsrc_t rw =
         __builtin_amdgcn_make_buffer_rsrc((void *)a.wp, (short)0, a.Kpad * a.Jpad, kBufFlags);
-    if (wave == NW - 1) {
+    if (grp == 0 && wave == NW - 1) {
         // records c0 .. c0 + TC - 1 (c0 + TC <= Kpad), a kilobyte per load;
         // older than this wave's stage loads, so every stage wait covers them
         const __amdgpu_buffer_rsrc_t rc =
@@ -196,13 +207,28 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
             voffB[i] = v ? pbase[i] + toff : kOutOfRange;
         }
     };
+    // one K-step of the loader: channel slice, then tap
+    auto advance = [&]() {
+        lc += BK;
+        if (lc == a.C) {
+            lc = 0;
+            if (++ls == a.S) {
+                ls = 0;
+                ++lr;   // lr == R past the last tap: every row reads out of range
+            }
+            set_tap();
+        }
+    };
+    // LDS buffer of a group's local stage ks (global K-step ks * KS + grp)
+    auto stage_buf = [&](int ks) { return lds + ((ks & (NSG - 1)) * KS + grp) * STAGE; };
     // Stages past the end are issued too (out of range: zeros, no memory
     // traffic), so every K-step waits for the same count.  Out of range is
     // signalled in the VGPR offset (>= 2^31) with a small scalar offset.
     auto issue = [&](int ks) {
-        int8_t *base = lds + (ks & (NS - 1)) * STAGE;
-        const bool live = ks < nk;
-        const int soffA = __builtin_amdgcn_readfirstlane(live ? ks * BK : 0);
+        int8_t *base = stage_buf(ks);
+        const int gs = ks * KS + grp;
+        const bool live = gs < nk;
+        const int soffA = __builtin_amdgcn_readfirstlane(live ? gs * BK : 0);
         const int oobA = __builtin_amdgcn_readfirstlane(live ? 0 : kOutOfRange);
         const int soffB = __builtin_amdgcn_readfirstlane(lc);
 #pragma unroll
@@ -216,15 +242,9 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
             set_tap();
             return;
         }
-        lc += BK;
-        if (lc == a.C) {
-            lc = 0;
-            if (++ls == a.S) {
-                ls = 0;
-                ++lr;   // lr == R past the last tap: every row reads out of range
-            }
-            set_tap();
-        }
+#pragma unroll
+        for (int q = 0; q < KS; ++q)
+            advance();
     };
 
     // ---- fragments and MFMAs ------------------------------------------
@@ -242,8 +262,8 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
     // wait for every stage in flight
     static_assert(FC + FP <= 15, "fragment reads of one step exceed the lgkmcnt range");
     auto read_frags = [&](int ks, v4i (&A)[FC], v4i (&B)[FP]) {
-        const int8_t *As = lds + (ks & (NS - 1)) * STAGE + (wc * WTC + lrow) * BK + co;
-        const int8_t *Bs = lds + (ks & (NS - 1)) * STAGE + TC * BK + (wpos * WTP + lrow) * BK + co;
+        const int8_t *As = stage_buf(ks) + (wc * WTC + lrow) * BK + co;
+        const int8_t *Bs = stage_buf(ks) + TC * BK + (wpos * WTP + lrow) * BK + co;
 #pragma unroll
         for (int i = 0; i < FC; ++i)
             A[i] = lds_read16(As + i * 16 * BK);
@@ -297,31 +317,38 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0, recs);
     } else {
         // ---- pipeline -----------------------------------------------------
-        // NS - 1 stages of loads in flight; the fragments of stage k + 1 are
-        // read from LDS while the MFMAs of stage k run.  The barrier of step
-        // k certifies that stage k + 1 has landed everywhere and that every
-        // wave is done with step k - 1, so buffer (k - 1) mod NS takes stage
-        // k + NS - 1.
+        // Per group, NSG - 1 stages of loads in flight; the fragments of its
+        // stage k + 1 are read from LDS while the MFMAs of its stage k run.
+        // The barrier of step k certifies that stage k + 1 of each group has
+        // landed everywhere and that every wave is done with step k - 1, so
+        // the group's buffer of local stage k - 1 takes stage k + NSG - 1.
+        // group grp starts at K-step grp; both groups run the same number of
+        // local steps (a step past the end reads zeros), so every barrier
+        // is reached by every wave
         set_tap();
+        for (int q = 0; q < grp; ++q)
+            advance();
+        const int nkl = (nk + KS - 1) / KS;
 #pragma unroll
-        for (int s = 0; s < NS - 1; ++s)
+        for (int s = 0; s < NSG - 1; ++s)
             issue(s);
-        stage_barrier<LPS *(NS - 2)>();
-        add_bconst<TC, TP, WC, WP, true>(acc, recs);   // the records landed with stage 0
+        stage_barrier<LPS *(NSG - 2)>();
+        if (grp == 0)
+            add_bconst<TC, TP, WC, WP, true>(acc, recs);   // the records landed with stage 0
         read_frags(0, fa[0], fb[0]);
         constexpr std::integral_constant<int, FC + FP> kNext{};
         int k = 0;
-        for (; k + 2 <= nk; k += 2) {
-            stage_barrier<LPS *(NS - 3)>();
-            issue(k + NS - 1);
+        for (; k + 2 <= nkl; k += 2) {
+            stage_barrier<LPS *(NSG - 3)>();
+            issue(k + NSG - 1);
             read_frags(k + 1, fa[1], fb[1]);
             mfma(kNext, fa[0], fb[0]);
-            stage_barrier<LPS *(NS - 3)>();
-            issue(k + NS);
+            stage_barrier<LPS *(NSG - 3)>();
+            issue(k + NSG);
             read_frags(k + 2, fa[0], fb[0]);
             mfma(kNext, fa[1], fb[1]);
         }
-        if (k < nk)
+        if (k < nkl)
             mfma(std::integral_constant<int, 0>{}, fa[0], fb[0]);
         // with an even step count the reads of step nk (past the last one)
         // are still in flight: retire them before their registers are
@@ -329,6 +356,26 @@ __global__ void __launch_bounds__(WC *WP * 64, (dma_occupancy<TC / WC, TP / WP>(
         lds_wait<0>();
         wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
         __syncthreads();
+        if constexpr (KS > 1) {
+            // the second group's partial sums, through LDS, into the first's
+            v4i *part = (v4i *)lds;
+            if (grp == 1) {
+#pragma unroll
+                for (int i = 0; i < FC; ++i)
+#pragma unroll
+                    for (int j = 0; j < FP; ++j)
+                        part[((wave * FC + i) * FP + j) * 64 + lane] = acc[i][j];
+            }
+            __syncthreads();
+            if (grp == 1)
+                return;   // the barriers below count only the first group
+#pragma unroll
+            for (int i = 0; i < FC; ++i)
+#pragma unroll
+                for (int j = 0; j < FP; ++j)
+                    acc[i][j] += part[((wave * FC + i) * FP + j) * 64 + lane];
+            __syncthreads();   // every partial read before the staging overwrites them
+        }
         store_tile<TC, TP, WC, WP, LDS_BYTES>(a, acc, lds, c0, p0, recs);
     }
 }
@@ -430,10 +477,12 @@ hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp
     return hipGetLastError();
 }
 
-// DmaTile -> tile, wave grid, stage count, short-reduction form.
+// DmaTile -> tile, wave grid, stage count, short-reduction form, K-step
+// groups.
 struct DmaCfg {
     int tc, tp, wc, wp, ns;
     bool sh;
+    int ks = 1;
 };
 static constexpr DmaCfg kDmaCfg[DMA_COUNT] = {
     {128, 128, 2, 2, 4, false}, {128, 128, 2, 2, 8, false}, {128, 64, 2, 2, 4, false},
@@ -444,7 +493,8 @@ static constexpr DmaCfg kDmaCfg[DMA_COUNT] = {
     {64, 128, 2, 2, 1, true},   {64, 64, 2, 2, 1, true},    {128, 128, 2, 2, 1, true},
     {128, 64, 2, 2, 1, true},   {64, 128, 2, 2, 2, true},   {128, 128, 2, 2, 2, true},
     {64, 64, 2, 2, 2, true},    {128, 64, 2, 2, 2, true},   {64, 128, 2, 2, 4, true},
-    {128, 128, 2, 2, 4, true},  {64, 64, 2, 2, 4, true},
+    {128, 128, 2, 2, 4, true},  {64, 64, 2, 2, 4, true},    {128, 64, 2, 2, 8, false, 2},
+    {64, 64, 2, 2, 8, false, 2}, {128, 128, 2, 2, 8, false, 2},
 };
 
 TileShape dma_tile_shape(int tile)
@@ -454,7 +504,12 @@ TileShape dma_tile_shape(int tile)
 
 int dma_threads(int tile)
 {
-    return kDmaCfg[tile].wc * kDmaCfg[tile].wp * 64;
+    return kDmaCfg[tile].wc * kDmaCfg[tile].wp * 64 * kDmaCfg[tile].ks;
+}
+
+int dma_split(int tile)
+{
+    return kDmaCfg[tile].ks;
 }
 
 int dma_stages(int tile)
@@ -474,12 +529,14 @@ static hipError_t launch_dma_cfg(const ConvArgs &a, hipStream_t st)
     const int grid = (a.ntiles + 7) / 8 * 8;
     if (c.sh && a.nk > c.ns)
         return hipErrorInvalidValue;   // more K-steps than the short form holds
+    if (c.ks > 1 && a.rowpack)
+        return hipErrorInvalidValue;   // the row-pair walk steps one K-step at a time
     if (a.flip4)
-        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, c.sh>), dim3(grid),
-                           dim3(c.wc * c.wp * 64), 0, st, a);
+        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, c.sh, c.ks>), dim3(grid),
+                           dim3(c.wc * c.wp * 64 * c.ks), 0, st, a);
     else
-        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, c.sh>), dim3(grid),
-                           dim3(c.wc * c.wp * 64), 0, st, a);
+        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, c.sh, c.ks>), dim3(grid),
+                           dim3(c.wc * c.wp * 64 * c.ks), 0, st, a);
     return hipGetLastError();
 }
 

@@ -346,9 +346,13 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
         for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_256x128_S4, DMA_128x256_S4,
                       DMA_128x128_S8, DMA_128x64_S8, DMA_64x64_S8, DMA_64x128_S8, DMA_64x64_S16})
             c.push_back({FAM_DMA, t});
+        // two K-step groups per tile: reductions of at least 8 steps
+        if ((J + 63) / 64 >= 8)
+            for (int t : {DMA_128x64_K2, DMA_64x64_K2, DMA_128x128_K2})
+                c.push_back({FAM_DMA, t});
         // short reductions: every K-step in flight at once
         for (int t = DMA_64x128_R1; t < DMA_COUNT; ++t)
-            if ((J + 63) / 64 <= dma_stages(t))
+            if (dma_short(t) && (J + 63) / 64 <= dma_stages(t))
                 c.push_back({FAM_DMA, t});
     }
     if (c.empty() || C4 % 64 != 0) {
@@ -815,14 +819,14 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     std::vector<ConvKernel> cands;
     if (rowpack) {
         const int f = env_int("QNN_DMA", -1);
-        if (f >= 0 && f < DMA_COUNT && (!dma_short(f) || npairs <= dma_stages(f))) {
+        if (f >= 0 && f < DMA_COUNT && dma_split(f) == 1 && (!dma_short(f) || npairs <= dma_stages(f))) {
             cands.push_back({FAM_DMA, f});
         } else {
             for (int t : {DMA_128x128_S4, DMA_128x64_S4, DMA_64x128_S4, DMA_64x64_S4, DMA_128x64_S8, DMA_64x128_S8,
                           DMA_64x64_S8})
                 cands.push_back({FAM_DMA, t});
             for (int t = DMA_64x128_R1; t < DMA_COUNT; ++t)
-                if (npairs <= dma_stages(t))
+                if (dma_short(t) && npairs <= dma_stages(t))
                     cands.push_back({FAM_DMA, t});
         }
     } else {

@@ -187,10 +187,15 @@ enum DmaTile {
     DMA_64x128_R4 = 23,
     DMA_128x128_R4 = 24,
     DMA_64x64_R4 = 25,
+    // two groups of 2x2 waves taking alternate K-steps, 8 stages (4 each)
+    DMA_128x64_K2 = 26,
+    DMA_64x64_K2 = 27,
+    DMA_128x128_K2 = 28,
     DMA_COUNT
 };
 TileShape dma_tile_shape(int tile);
 int dma_threads(int tile);
+int dma_split(int tile);    // K-step groups sharing a tile (1 or 2)
 int dma_stages(int tile);
 bool dma_short(int tile);   // short-reduction form: at most dma_stages(tile) K-steps
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);

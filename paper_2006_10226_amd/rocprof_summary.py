@@ -24,7 +24,7 @@ import re
 
 _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
 _TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
-_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)>")
+_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)(?:, ?(\d+))?>")
 _WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
 _HALO = re.compile(r"conv_halo_kernel<(\d+), ?(true|false)>")
 _WIN = re.compile(r"conv_window_kernel<(\d+), ?(\d+), ?(\d+), ?(true|false)>")
@@ -60,7 +60,8 @@ def group_of(kernel_name):
     if m:
         tc, tp, wc, wp, ns = (int(v) for v in m.groups()[:5])
         short = "s" if m.group(7) == "true" else ""
-        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * 64} stages={ns}{short}"
+        ks = int(m.group(8)) if m.group(8) else 1
+        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * ks * 64} stages={ns}{short}"
     m = _WAVE.search(kernel_name)
     if m:
         split = int(m.group(1))

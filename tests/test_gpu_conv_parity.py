@@ -330,11 +330,14 @@ SHORT_SHAPES = [
     (W.ConvLayer("s", 6, 6, 192, 64, 1, 1), 3, {}),
     (W.ConvLayer("s", 10, 10, 128, 130, 1, 1), 2, dict(yt="i32")),
 ]
-# K-steps each LDS-direct configuration holds in its short form (0: ring)
-DMA_SHORT_STAGES = [0] * 15 + [1, 1, 1, 1, 2, 2, 2, 2, 4, 4, 4]
+# K-steps each LDS-direct configuration holds in its short form (0: ring);
+# the last three are ring forms with two K-step groups per tile (the
+# shapes above have 4, 9, 14 and 18 K-steps: odd counts leave the second
+# group a step past the end)
+DMA_SHORT_STAGES = [0] * 15 + [1, 1, 1, 1, 2, 2, 2, 2, 4, 4, 4] + [0, 0, 0]
 
 
-@pytest.mark.parametrize("tile", list(range(26)))
+@pytest.mark.parametrize("tile", list(range(len(DMA_SHORT_STAGES))))
 def test_every_dma_tile(tile):
     short = DMA_SHORT_STAGES[tile]
     shapes = TAP_SHAPES if not short else [sh for sh in SHORT_SHAPES if (sh[0].Cin + 63) // 64 <= short]
@@ -350,6 +353,21 @@ def test_every_dma_tile(tile):
         c = W.conv_case(shapes[0][0], 2, seed=7)
         c.zp_x = 0
         assert_equal(run_gpu(c), run_oracle(c), f"dma tile {tile} zp_x 0")
+
+
+@pytest.mark.parametrize("tile", [26, 27, 28])
+def test_split_dma_tiles_skip_row_pair_stem(tile):
+    """The two-group tiles step the activations by two K-steps; the row-pair
+    walk of a 3-channel stem steps one row pair at a time, so a forced
+    two-group tile is not used there and the plan takes its own choice."""
+    layer = W.ConvLayer("stem", 30, 30, 3, 64, 7, 7, 2, (3, 3, 3, 3))
+    c = W.conv_case(layer, 2, seed=tile)
+    with env(QNN_DMA=tile):
+        p, keep = make_plan(c)
+        d = p.describe()
+        p.close()
+        assert "threads=512" not in d, d
+        assert_equal(run_gpu(c), run_oracle(c), f"stem with dma {tile} forced")
 
 
 @pytest.mark.parametrize("layer,tile", [
