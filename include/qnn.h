@@ -72,9 +72,14 @@ typedef enum {
 typedef enum { QNN_UINT8 = 0, QNN_INT8 = 1, QNN_INT32 = 2 } qnn_dtype;
 
 /* Rounding of the fixed-point requantize (the paper leaves it to the
- * framework, Sec. III-B): HALF_UP rounds ties toward +infinity, HALF_AWAY
- * rounds ties away from zero. */
-typedef enum { QNN_ROUND_HALF_UP = 0, QNN_ROUND_HALF_AWAY = 1 } qnn_rounding;
+ * framework, Sec. III-B): HALF_UP rounds round(v * mult / 2^shift) with ties
+ * toward +infinity, HALF_AWAY with ties away from zero.  TWO_STAGE is the
+ * integer-only form of Jacob et al. used by pre-quantized TFLite models:
+ * for shift >= 31 the product is divided by 2^31 rounding half up, and that
+ * integer by 2^(shift - 31) rounding half away from zero (two roundings,
+ * so a result may differ by 1 from either single rounding); for shift < 31
+ * (multipliers of 1 or more) one half-up rounding. */
+typedef enum { QNN_ROUND_HALF_UP = 0, QNN_ROUND_HALF_AWAY = 1, QNN_ROUND_TWO_STAGE = 2 } qnn_rounding;
 
 /* Quantization attributes of one tensor (host arrays).  n == 1: per tensor;
  * n == channel count: per output channel (weights) or per innermost channel

@@ -12,7 +12,10 @@ Sec. II-B Eq. (2)/(3), Sec. III-B Eq. (5)):
   * a quantized tensor is (Q, scale, zero_point); the weight scale and zero
     point are per tensor (length 1) or per output channel;
   * bias is int32 with implied scale s_x * s_w[k] and zero point 0;
-  * rounding "half_up" (ties toward +inf) or "half_away" (ties away from 0).
+  * rounding "half_up" (ties toward +inf), "half_away" (ties away from 0) or
+    "two_stage" (for shifts of 31 or more: divide by 2^31 rounding half up,
+    then by 2^(shift - 31) rounding half away from zero; Jacob et al.'s
+    integer-only form).
 """
 from __future__ import annotations
 
@@ -26,7 +29,7 @@ _LIB_PATH = os.path.join(_HERE, "libqnn_oracle.so")
 
 DTYPE_CODE = {np.dtype(np.uint8): 0, np.dtype(np.int8): 1, np.dtype(np.int32): 2}
 NAME_TO_NP = {"u8": np.uint8, "i8": np.int8, "i32": np.int32}
-ROUNDING = {"half_up": 0, "half_away": 1}
+ROUNDING = {"half_up": 0, "half_away": 1, "two_stage": 2}
 DTYPE_RANGE = {"u8": (0, 255), "i8": (-128, 127), "i32": (-(2**31), 2**31 - 1)}
 
 _lib = None

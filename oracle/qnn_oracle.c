@@ -26,9 +26,14 @@
  *     e + 1 when it reaches 2^31, shift n = 31 - e; the result is
  *     round(v * mult / 2^n) under the selected rounding, then + zp_out, then
  *     saturation to the output range intersected with the activation clamp.
- *     The paper leaves the rounding open ("different frameworks choose
- *     different rounding methods"); two are defined: HALF_UP (ties toward
- *     +infinity) and HALF_AWAY (ties away from zero).
+ *     The paper leaves the rounding open to the framework; three are
+ *     defined: HALF_UP (ties toward +infinity), HALF_AWAY (ties away from
+ *     zero) and TWO_STAGE, the integer-only form of Jacob et al. (the
+ *     paper's reference for pre-quantized TFLite models): for n >= 31 the
+ *     product is first divided by 2^31 and rounded half up (a rounding
+ *     high multiply), that result then divided by 2^(n - 31) and rounded
+ *     half away from zero (a rounding right shift); for n < 31 a single
+ *     half-up rounding.
  *   - qnn.add: each input is requantized to the output scale (without its
  *     own output zero point), the two are added, then zp_out and the clamp.
  *
@@ -48,6 +53,7 @@
 
 #define ORACLE_HALF_UP 0
 #define ORACLE_HALF_AWAY 1
+#define ORACLE_TWO_STAGE 2
 
 /* Read element i of a quantized tensor of dtype dt, widened to int64. */
 static int64_t q_load(const void *p, int dt, int64_t i)
@@ -144,8 +150,19 @@ int64_t oracle_round_mul_shift(int64_t v, int32_t mult, int32_t shift, int round
     int64_t p = v * (int64_t)mult;
     if (shift >= 63)
         return 0; /* |p| < 2^62, so |p| / 2^shift < 1/2 */
+    if (rounding == ORACLE_TWO_STAGE && shift >= 31) {
+        /* stage 1: p / 2^31 rounded half up */
+        int64_t x1 = floor_div_pow2(p + ((int64_t)1 << 30), 31);
+        int e = shift - 31;
+        if (e == 0)
+            return x1;
+        /* stage 2: x1 / 2^e rounded half away from zero */
+        int64_t m = x1 < 0 ? -x1 : x1;
+        int64_t r = floor_div_pow2(m + ((int64_t)1 << (e - 1)), e);
+        return x1 < 0 ? -r : r;
+    }
     int64_t half = (int64_t)1 << (shift - 1);
-    if (rounding == ORACLE_HALF_UP)
+    if (rounding == ORACLE_HALF_UP || rounding == ORACLE_TWO_STAGE)
         return floor_div_pow2(p + half, shift);
     /* HALF_AWAY: round the magnitude half up, then restore the sign */
     int64_t a = p < 0 ? -p : p;

@@ -34,15 +34,6 @@ __device__ __forceinline__ int fast_div(int n, uint32_t mul, uint32_t shift)
     return mul ? (int)(__umulhi((uint32_t)n, mul) >> shift) : n;
 }
 
-// round(v * mult / 2^shift), 64-bit product; HALF_UP adds 2^(shift-1) and
-// floors, HALF_AWAY adds one less for negative products.
-__device__ __forceinline__ long long round_mul_shift64(int v, int mult, int shift, int away)
-{
-    const long long p = (long long)v * (long long)mult;
-    const long long bias = (1LL << (shift - 1)) - (long long)(away & (int)((unsigned long long)p >> 63));
-    return (p + bias) >> shift;
-}
-
 // Requantize four accumulators of consecutive channels (records rec[e] =
 // {mult, bconst, rndzp, shift}) and pack the output bytes.  The 32-bit form
 // (HALF_UP, 33 <= shift <= 53) is exact: with hi the signed high word of
@@ -65,7 +56,7 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int v = (int)((uint32_t)acc[e] + (uint32_t)rec[e].y);   // wraps exactly when the sum fits
-        long long o = round_mul_shift64(v, rec[e].x, rec[e].w, a.rounding) + a.zp_y;
+        long long o = rounding_mul_shift(v, rec[e].x, rec[e].w, a.rounding) + a.zp_y;
         o = o < a.lo ? a.lo : (o > a.hi ? a.hi : o);
         packed |= ((uint32_t)o & 0xffu) << (8 * e);
     }

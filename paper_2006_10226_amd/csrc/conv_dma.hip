@@ -118,8 +118,8 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave_id = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
-    const int grp = wave_id / NW;     // K-step group: steps grp, grp + KS, ...
-    const int wave = wave_id % NW;    // wave inside its group
+    const int grp = KS == 1 ? 0 : wave_id / NW;         // K-step group: steps grp, grp + KS, ...
+    const int wave = KS == 1 ? wave_id : wave_id % NW;   // wave inside its group
     const int wc = wave / WP, wpos = wave % WP;
 
     // XCD x (workgroups dealt round-robin) takes the x-th eighth of the

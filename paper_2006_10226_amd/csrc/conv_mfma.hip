@@ -60,17 +60,6 @@ __device__ __forceinline__ int swizzle(int row)
         return ((row >> 1) & 3) ^ ((row >> 3) & 1);
 }
 
-// Fixed-point requantize of v: round(v * mult / 2^shift) as a 64-bit product
-// (|v| <= 2^31, mult < 2^31, 1 <= shift <= 63).  HALF_UP adds 2^(shift-1)
-// and floors; HALF_AWAY differs only for negative products, where one less
-// is added (ties then go down, i.e. away from zero).
-__device__ __forceinline__ long long round_mul_shift(int v, int mult, int shift, int away)
-{
-    const long long p = (long long)v * (long long)mult;
-    const long long bias = (1LL << (shift - 1)) - (long long)(away & (int)((unsigned long long)p >> 63));
-    return (p + bias) >> shift;
-}
-
 // The 32-bit form used by the conv epilogue when rounding is HALF_UP and
 // 33 <= shift <= 53: with hi = floor(v*mult / 2^32) (the signed high word of
 // the product) and sh = shift - 32,
@@ -378,7 +367,7 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
                     packed = 0;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const int o = clamp_i(round_mul_shift(vals[e], mult[e], shift[e], a.rounding) + a.zp_y, a.lo,
+                        const int o = clamp_i(rounding_mul_shift(vals[e], mult[e], shift[e], a.rounding) + a.zp_y, a.lo,
                                               a.hi);
                         packed |= ((uint32_t)o & 0xffu) << (8 * e);
                     }
@@ -446,7 +435,8 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const int v = (int)((uint32_t)acc[i][jj][e] + (uint32_t)bconst[e]);
-                        const int o = clamp_i(round_mul_shift(v, mult[e], shift[e], a.rounding) + a.zp_y, a.lo, a.hi);
+                        const int o =
+                            clamp_i(rounding_mul_shift(v, mult[e], shift[e], a.rounding) + a.zp_y, a.lo, a.hi);
                         packed |= ((uint32_t)o & 0xffu) << (8 * e);
                     }
                 }

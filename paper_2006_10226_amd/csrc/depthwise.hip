@@ -40,17 +40,6 @@ __device__ __forceinline__ int dot4(uint32_t a, uint32_t b, int c)
 // 12 a zero byte
 constexpr uint32_t kZero = 0x0c;
 
-__device__ __forceinline__ long long rms64(int v, int mult, int shift, int rounding)
-{
-    const long long p = (long long)v * (long long)mult;
-    const long long half = 1LL << (shift - 1);
-    if (rounding == 0)
-        return (p + half) >> shift;
-    const long long m = p < 0 ? -p : p;
-    const long long t = (m + half) >> shift;
-    return p < 0 ? -t : t;
-}
-
 }  // namespace
 
 // output pixels per work item
@@ -181,7 +170,7 @@ __global__ void __launch_bounds__(256) depthwise3_kernel(DwArgs a)
         } else {
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
-                long long o = rms64(v[c], cr[c].mult, cr[c].shift, a.rounding) + a.zp_y;
+                long long o = rounding_mul_shift(v[c], cr[c].mult, cr[c].shift, a.rounding) + a.zp_y;
                 o = o < a.lo ? a.lo : (o > a.hi ? a.hi : o);
                 packed[c >> 2] |= ((uint32_t)o & 0xffu) << (8 * (c & 3));
             }

@@ -13,17 +13,6 @@
 
 namespace qnn {
 
-__device__ __forceinline__ long long rms(int v, int mult, int shift, int rounding)
-{
-    long long p = (long long)v * (long long)mult;
-    long long half = 1LL << (shift - 1);
-    if (rounding == 0)
-        return (p + half) >> shift;
-    long long a = p < 0 ? -p : p;
-    long long t = (a + half) >> shift;
-    return p < 0 ? -t : t;
-}
-
 __device__ __forceinline__ int clampll(long long v, int lo, int hi)
 {
     return (int)(v < lo ? lo : (v > hi ? hi : v));
@@ -86,7 +75,7 @@ __global__ void __launch_bounds__(256) depthwise_kernel(DwArgs a)
         for (int e = 0; e < CV; ++e) {
             const ChanRec cr = a.chan[c + e];
             const int v = (int)((uint32_t)acc[e] + (uint32_t)cr.bconst);
-            yp[e] = (uint8_t)clampll(rms(v, cr.mult, cr.shift, a.rounding) + a.zp_y, a.lo, a.hi);
+            yp[e] = (uint8_t)clampll(rounding_mul_shift<true>(v, cr.mult, cr.shift, a.rounding) + a.zp_y, a.lo, a.hi);
         }
     }
 }
@@ -193,7 +182,7 @@ __device__ __forceinline__ int req_one(const ReqArgs &a, int q, int c)
         const int4 t = *(const int4 *)(a.tab + 4 * c);
         mult = t.x; shift = t.y; zi = t.z; zo = t.w;
     }
-    return clampll(rms(q - zi, mult, shift, a.rounding) + zo, a.lo, a.hi);
+    return clampll(rounding_mul_shift<true>(q - zi, mult, shift, a.rounding) + zo, a.lo, a.hi);
 }
 
 // Each thread handles groups of 16 elements (vector loads/stores when the
@@ -228,7 +217,8 @@ __global__ void __launch_bounds__(256) requantize_kernel(ReqArgs a)
 
 __device__ __forceinline__ int add_one(const AddArgs &a, int x, int y)
 {
-    const long long t = rms(x - a.zpa, a.ma, a.na, a.rounding) + rms(y - a.zpb, a.mb, a.nb, a.rounding);
+    const long long t = rounding_mul_shift<true>(x - a.zpa, a.ma, a.na, a.rounding) +
+                        rounding_mul_shift<true>(y - a.zpb, a.mb, a.nb, a.rounding);
     return clampll(t + a.zp_y, a.lo, a.hi);
 }
 

@@ -214,7 +214,7 @@ qnn_status validate_conv(const ConvDesc &d, int32_t *Ho, int32_t *Wo, int32_t *l
         return fail(QNN_ERR_DTYPE, "%s: input dtype must be uint8 or int8", op);
     if (d.yt != QNN_UINT8 && d.yt != QNN_INT8 && d.yt != QNN_INT32)
         return fail(QNN_ERR_DTYPE, "%s: output dtype must be uint8, int8 or int32", op);
-    if (d.rnd != QNN_ROUND_HALF_UP && d.rnd != QNN_ROUND_HALF_AWAY)
+    if (d.rnd < QNN_ROUND_HALF_UP || d.rnd > QNN_ROUND_TWO_STAGE)
         return fail(QNN_ERR_QPARAM, "%s: unknown rounding %d", op, (int)d.rnd);
     if (d.N < 0 || d.H < 1 || d.W < 1 || d.C < 1 || d.K < 1 || d.R < 1 || d.S < 1)
         return fail(QNN_ERR_SHAPE, "%s: sizes must be positive (N >= 0)", op);
@@ -1184,7 +1184,7 @@ qnn_status make_req_plan(qnn_dtype xt, int64_t count, int32_t channels, qnn_qpar
         return fail(QNN_ERR_DTYPE, "requantize: unknown input dtype");
     if (yt != QNN_UINT8 && yt != QNN_INT8 && yt != QNN_INT32)
         return fail(QNN_ERR_DTYPE, "requantize: unknown output dtype");
-    if (rnd != QNN_ROUND_HALF_UP && rnd != QNN_ROUND_HALF_AWAY)
+    if (rnd < QNN_ROUND_HALF_UP || rnd > QNN_ROUND_TWO_STAGE)
         return fail(QNN_ERR_QPARAM, "requantize: unknown rounding %d", (int)rnd);
     if (count < 0 || channels < 1 || count % channels != 0)
         return fail(QNN_ERR_SHAPE, "requantize: count must be a non-negative multiple of channels >= 1");
@@ -1357,7 +1357,7 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
         return fail(QNN_ERR_DTYPE, "add: b must be uint8 or int8");
     if (y_dtype != QNN_UINT8 && y_dtype != QNN_INT8)
         return fail(QNN_ERR_DTYPE, "add: y must be uint8 or int8");
-    if (rounding != QNN_ROUND_HALF_UP && rounding != QNN_ROUND_HALF_AWAY)
+    if (rounding < QNN_ROUND_HALF_UP || rounding > QNN_ROUND_TWO_STAGE)
         return fail(QNN_ERR_QPARAM, "add: unknown rounding %d", (int)rounding);
     if (count < 0)
         return fail(QNN_ERR_SHAPE, "add: count must be >= 0");

@@ -24,6 +24,40 @@ struct ChanRec {
 
 enum OutMode { OUT_REQUANT = 0, OUT_INT32 = 1 };
 
+// Fixed-point requantize of v: round(v * mult / 2^shift) with a 64-bit
+// product (|v| <= 2^31, 0 <= mult < 2^31, 1 <= shift <= 63); the mode is the
+// public qnn_rounding value.
+//   0 HALF_UP: floor((p + 2^(shift-1)) / 2^shift), ties toward +infinity;
+//   1 HALF_AWAY: one less is added for negative products, ties away from 0;
+//   2 TWO_STAGE (shift >= 31): a rounding high multiply, x1 = floor((p +
+//     2^30) / 2^31) (ties up), then x1 / 2^(shift - 31) rounded with ties
+//     away from zero (one less added for negative x1), so a product may be
+//     rounded twice; for shift < 31 (multipliers of 1 or more) one rounding,
+//     as HALF_UP.
+// Both code shapes compute the same value; which one leaves a kernel fewer
+// registers (and so more resident waves) depends on the kernel: the
+// elementwise kernels take the early HALF_UP return (EARLY = true), the
+// conv epilogues the single shared rounding.
+template <bool EARLY = false>
+__device__ __forceinline__ long long rounding_mul_shift(int v, int mult, int shift, int mode)
+{
+    long long p = (long long)v * (long long)mult;
+    if constexpr (EARLY) {
+        if (mode == 0)
+            return (p + (1LL << (shift - 1))) >> shift;
+    }
+    if (mode == 2) {
+        if (shift > 31) {
+            p = (p + (1LL << 30)) >> 31;   // stage 1: / 2^31, ties up
+            shift -= 31;                   // stage 2 below: ties away from zero
+            mode = 1;
+        } else {
+            mode = 0;                      // one rounding, ties up
+        }
+    }
+    return (p + (1LL << (shift - 1)) - (mode == 1 && p < 0 ? 1 : 0)) >> shift;
+}
+
 // min(max(t, lo), hi) for lo <= hi (the host rejects empty clamps) in one
 // VALU operation; the compiler emits a max and a min for runtime bounds.
 __device__ __forceinline__ int clamp_i32(int t, int lo, int hi)

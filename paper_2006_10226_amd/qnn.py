@@ -23,11 +23,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libqnn.so")
 
 UINT8, INT8, INT32 = 0, 1, 2
-HALF_UP, HALF_AWAY = 0, 1
+HALF_UP, HALF_AWAY, TWO_STAGE = 0, 1, 2
 _TORCH_DT = {torch.uint8: UINT8, torch.int8: INT8, torch.int32: INT32}
 _NAME_DT = {"u8": UINT8, "i8": INT8, "i32": INT32}
 _DT_TORCH = {UINT8: torch.uint8, INT8: torch.int8, INT32: torch.int32}
-_ROUND = {"half_up": HALF_UP, "half_away": HALF_AWAY}
+_ROUND = {"half_up": HALF_UP, "half_away": HALF_AWAY, "two_stage": TWO_STAGE}
 INT32_MIN, INT32_MAX = -(2**31), 2**31 - 1
 
 STATUS = ["QNN_OK", "QNN_ERR_NULL", "QNN_ERR_SHAPE", "QNN_ERR_DTYPE", "QNN_ERR_QPARAM",

@@ -117,6 +117,17 @@ def round_half_away(q: Fraction) -> int:
     return -m if q < 0 else m
 
 
+def round_two_stage(p: int, shift: int) -> int:
+    """Jacob et al.'s integer-only requantize of the product p = v * mult for
+    a right shift `shift`: for shift >= 31, p / 2^31 rounded half up, then
+    that integer / 2^(shift - 31) rounded half away from zero; for shift < 31
+    one rounding, half up."""
+    if shift < 31:
+        return round_half_up(Fraction(p, 2**shift))
+    x1 = round_half_up(Fraction(p, 2**31))
+    return round_half_away(Fraction(x1, 2**(shift - 31)))
+
+
 ROUND = {"half_up": round_half_up, "half_away": round_half_away}
 
 

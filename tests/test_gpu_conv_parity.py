@@ -32,6 +32,13 @@ def test_dense_bert_ffn(layer, seed):
     assert_equal(run_gpu(c, one_shot=True), run_oracle(c), layer.name + " one-shot")
 
 
+def test_dense_two_stage_rounding():
+    c = W.dense_case(W.bert_ffn()[0], 7)
+    c.rounding = "two_stage"
+    log("dense two-stage")
+    assert_equal(run_gpu(c), run_oracle(c), "dense two-stage")
+
+
 def test_resnet50_batch1_full():
     for i, layer in enumerate(W.resnet50()):
         c = W.conv_case(layer, 1, seed=3000 + i)
@@ -182,6 +189,18 @@ VARIANTS = [
     ("dw_5x5_i32", W.ConvLayer("v", 9, 9, 16, 16, 5, 5, 1, (2, 2, 2, 2), depthwise=True), 2, dict(yt="i32")),
     ("dw_half_away", W.ConvLayer("v", 8, 8, 64, 64, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2,
      dict(rounding="half_away")),
+    # the two-stage rounding through every epilogue: the LDS-direct / tap
+    # kernels (3x3, C % 64 == 0), the short 1x1 form, the gather kernel (C
+    # not a multiple of 64), the dot-product depthwise kernel and the
+    # general one, int8 and uint8 outputs
+    ("two_stage", W.ConvLayer("v", 10, 10, 64, 64, 3, 3, 1, (1, 1, 1, 1)), 2, dict(rounding="two_stage")),
+    ("two_stage_1x1_i8", W.ConvLayer("v", 9, 9, 256, 100, 1, 1), 3, dict(rounding="two_stage", yt="i8")),
+    ("two_stage_gather", W.ConvLayer("v", 9, 9, 20, 36, 3, 3, 1, (1, 1, 1, 1)), 2, dict(rounding="two_stage")),
+    ("two_stage_deep", W.ConvLayer("v", 7, 7, 512, 64, 3, 3, 1, (1, 1, 1, 1)), 2, dict(rounding="two_stage")),
+    ("dw_two_stage", W.ConvLayer("v", 8, 8, 64, 64, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2,
+     dict(rounding="two_stage")),
+    ("dw_5x5_two_stage", W.ConvLayer("v", 9, 9, 16, 16, 5, 5, 1, (2, 2, 2, 2), depthwise=True), 2,
+     dict(rounding="two_stage", yt="i8")),
 ]
 
 
@@ -221,7 +240,7 @@ def test_random_shapes():
         pads = tuple(int(v) for v in rng.integers(0, 3, size=4))
         layer = W.ConvLayer("r", H, Wd, C, K, R, S, st, pads)
         kw = dict(zp_w=str(rng.choice(["zero", "tensor", "channel"])),
-                  rounding=str(rng.choice(["half_up", "half_away"])),
+                  rounding=str(rng.choice(["half_up", "half_away", "two_stage"])),
                   x_dtype=str(rng.choice(["u8", "i8"])), yt=str(rng.choice(["u8", "i8", "i32"])),
                   bias=bool(rng.integers(0, 2)))
         c = W.conv_case(layer, int(rng.integers(1, 4)), seed=t, **kw)

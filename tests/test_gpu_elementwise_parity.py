@@ -38,7 +38,7 @@ def test_requantize(xt, yt, perch):
         zp_in = np.zeros(n, np.int32) if xt == "i32" else _draw(rng, xt, n).astype(np.int32)
         s_out = (10.0 ** rng.uniform(-3, -1, size=n)).astype(np.float32)
         zp_out = np.zeros(n, np.int32) if yt == "i32" else _draw(rng, yt, n).astype(np.int32)
-        for rounding in ("half_up", "half_away"):
+        for rounding in ("half_up", "half_away", "two_stage"):
             log(f"requantize {xt}->{yt} perch={perch} {shape} {rounding}")
             act = None if yt == "i32" else (int(zp_out.min()), _RANGE[yt][1] - 1)
             y = Q.requantize(dev(x), s_in, zp_in, s_out, zp_out, yt, act, rounding).cpu().numpy()
@@ -79,8 +79,24 @@ def test_add_variants(at, bt, yt):
         a, b = _draw(rng, at, count), _draw(rng, bt, count)
         za, zb = int(_draw(rng, at, 1)[0]), int(_draw(rng, bt, 1)[0])
         zo = int(_draw(rng, yt, 1)[0])
-        for rounding in ("half_up", "half_away"):
+        for rounding in ("half_up", "half_away", "two_stage"):
             act = (zo, _RANGE[yt][1] - 1)
             y = Q.add(dev(a), 0.013, za, dev(b), 0.3, zb, 0.021, zo, yt, act, rounding).cpu().numpy()
             ref = O.add(a, 0.013, za, b, 0.3, zb, 0.021, zo, yt, act, rounding)
             assert_equal(y, ref, f"add {at}+{bt}->{yt} n={count}")
+
+
+@pytest.mark.parametrize("yt", ["i8", "i32"])
+def test_requantize_two_stage_ties(yt):
+    """Scale ratios 1/4, 3/8 and 5/1024 put many products on a tie of the
+    first or the second rounding, where the two-stage result differs from
+    one half-up rounding; the GPU follows the oracle on every one."""
+    rng = np.random.default_rng(21)
+    x = rng.integers(-500, 500, size=(4099,), dtype=np.int64).astype(np.int32)   # int8 results mostly unclamped
+    differs = 0
+    for s_in, s_out in [(0.25, 1.0), (0.375, 1.0), (5.0, 1024.0)]:
+        y = Q.requantize(dev(x), s_in, 0, s_out, 0, yt, None, "two_stage").cpu().numpy()
+        ref = O.requantize(x, s_in, 0, s_out, 0, yt, None, "two_stage")
+        assert_equal(y, ref, f"two-stage ties {s_in}/{s_out}")
+        differs += int((ref != O.requantize(x, s_in, 0, s_out, 0, yt, None, "half_up")).sum())
+    assert differs > 1000

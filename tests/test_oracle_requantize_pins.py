@@ -214,3 +214,61 @@ def test_add_against_fraction_per_term(oracle):
         ta = X.round_half_up(Fraction((int(case.a.flat[i]) - case.zp_a) * ma, 2**na))
         tb = X.round_half_up(Fraction((int(case.b.flat[i]) - case.zp_b) * mb, 2**nb))
         assert int(y.flat[i]) == min(255, max(0, case.zp_o + ta + tb))
+
+
+# ---- the two-stage rounding (Jacob et al.'s integer-only requantize) ----
+
+def test_two_stage_worked_example(oracle):
+    """v = 9, M = 2^30 / 2^32 = 1/4: one rounding gives round(2.25) = 2; two
+    stages give 9 * 2^30 / 2^31 = 4.5 -> 5 (half up), then 5 / 2 = 2.5 -> 3
+    (half away).  v = -9: -4.5 -> -4, -4 / 2 = -2.  v = 7: 3.5 -> 4, 4 / 2 = 2
+    (equal to one rounding of 1.75)."""
+    m, s = 2**30, 32
+    assert oracle.round_mul_shift(9, m, s, "two_stage") == 3
+    assert oracle.round_mul_shift(9, m, s, "half_up") == 2
+    assert oracle.round_mul_shift(-9, m, s, "two_stage") == -2
+    assert oracle.round_mul_shift(7, m, s, "two_stage") == 2
+    # stage 2 rounds ties away from zero: -6 * 2^30 / 2^31 = -3 exactly,
+    # then -3 / 2 = -1.5 -> -2 (one half-up rounding of -1.5 gives -1)
+    assert oracle.round_mul_shift(-6, m, s, "two_stage") == -2
+    assert oracle.round_mul_shift(-6, m, s, "half_up") == -1       # -1.5 -> -1
+    # shift 31: stage 2 divides by 1, one half-up rounding of v * mult / 2^31
+    assert oracle.round_mul_shift(3, 2**30, 31, "two_stage") == 2   # 1.5 -> 2
+    assert oracle.round_mul_shift(-3, 2**30, 31, "two_stage") == -1  # -1.5 -> -1
+
+
+def test_two_stage_exact_rational(oracle):
+    """Against the two exact-rational roundings for dense small values, int32
+    extremes, constructed stage-1 and stage-2 ties and many multipliers
+    (shifts below 31 are one half-up rounding)."""
+    rng = np.random.default_rng(12)
+    dense = list(range(-3000, 3001, 3))
+    extremes = [2**31 - 1, -(2**31), -(2**31) + 1, 2**30, -(2**30), 2**31]
+    Ms = [0.5, 0.25, 2.0**-11, 0.75, 0.002, 1.0 / 3.0, 1.5, 3.0, 1000.0] + _multipliers(rng, 30)
+    for M in Ms:
+        mult, shift = oracle.quantize_multiplier(M)
+        for v in dense + extremes + rng.integers(-(2**31), 2**31, size=200).tolist():
+            got = oracle.round_mul_shift(v, mult, shift, "two_stage")
+            assert got == X.round_two_stage(v * mult, shift), (M, v)
+    # ties at each stage: mult = 2^30 makes v * mult / 2^31 = v / 2
+    for shift in range(31, 45):
+        for v in range(-200, 201):
+            assert oracle.round_mul_shift(v, 2**30, shift, "two_stage") == X.round_two_stage(v * 2**30, shift)
+
+
+def test_two_stage_within_one_of_single_rounding(oracle):
+    """Two roundings stay within 1 of one rounding of the same product."""
+    rng = np.random.default_rng(13)
+    for M in _multipliers(rng, 20):
+        mult, shift = oracle.quantize_multiplier(M)
+        for v in rng.integers(-(2**31), 2**31, size=300).tolist():
+            a = oracle.round_mul_shift(v, mult, shift, "two_stage")
+            b = oracle.round_mul_shift(v, mult, shift, "half_up")
+            assert abs(a - b) <= 1, (M, v)
+
+
+def test_two_stage_requantize_monotone(oracle):
+    v = np.arange(-70000, 70001, 7, dtype=np.int32)
+    for s_in, s_out, zp, yt in [(0.001, 0.05, 3, "u8"), (0.0123, 0.5, -3, "i8"), (0.3, 0.2, 0, "i32")]:
+        y = oracle.requantize(v, s_in, 0, s_out, zp, yt, None, "two_stage").astype(np.int64)
+        assert (np.diff(y) >= 0).all()
