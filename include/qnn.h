@@ -15,7 +15,7 @@
  *     scale_A * scale_B and zero point 0; Eq. (3) splits it into four terms.
  *   - Sec. III-B: padding uses the input zero point; requantize (Eq. (5))
  *     maps a quantized tensor to another (scale, zero_point) with a
- *     fixed-point multiplier; the rounding is a choice (two are offered).
+ *     fixed-point multiplier; the rounding is a choice (three are offered).
  *   - Sec. III-A, Fig. 2: a framework conv is qnn.conv2d -> bias_add -> clip
  *     -> requantize; here the clip is applied in the output Q domain after
  *     requantize (identical for ReLU).
