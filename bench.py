@@ -13,7 +13,10 @@ dominant kernel, and the CPU oracle timed on a bounded sample.
 
 Other workloads (--workload): mobilenet_v2_b64, inception_v3_b64, dense_bert,
 conv14x14x64 -- the same measurement on those layer sets (depthwise layers
-and adds are reported in GB/s in the per-layer file).
+and adds are reported in GB/s in the per-layer file); resnet50_b32_chain --
+the 16 bottleneck blocks chained as in the network (each conv reads the int8
+tensor its producer wrote, a qnn.add closes every block; 52 convs and 16 adds,
+the stem left out), TOP/s over the convs' MACs and the whole chain's time.
 """
 import argparse
 import json
@@ -85,10 +88,52 @@ class Item:
     pass
 
 
+def setup_chain(N):
+    """Plans and device tensors of the chained bottleneck blocks: every step
+    writes its own output tensor, which its consumers read."""
+    import torch
+    import workloads as W
+    from paper_2006_10226_amd import qnn as Q
+
+    ch = W.resnet50_chain(N)
+    t = {"x0": torch.from_numpy(ch.x0).cuda()}
+    items = []
+    for st in ch.steps:
+        it = Item()
+        if isinstance(st, W.ChainConv):
+            L = st.layer
+            s_x, zp_x = ch.q[st.src]
+            it.kind, it.layer, it.name = "conv", L, L.name
+            it.w, it.bias = torch.from_numpy(st.w).cuda(), torch.from_numpy(st.bias).cuda()
+            it.plan = Q.conv2d_plan(tuple(t[st.src].shape), "i8", s_x, zp_x, it.w, st.s_w, st.zp_w, it.bias,
+                                    L.stride, L.pads, 1, st.s_y, st.zp_y, "i8", st.act)
+            it.x = t[st.src]
+            it.out = t[st.dst] = it.plan.new_output()
+            it.desc = it.plan.describe()
+            Nb, Ho, Wo, K = it.plan.out_shape
+            it.macs = Nb * Ho * Wo * K * L.R * L.S * L.Cin
+            it.bytes = it.x.numel() + st.w.size + it.out.numel()
+            it.run = (lambda it=it: it.plan.run(it.x, it.out))
+        else:
+            s_a, zp_a = ch.q[st.a]
+            s_b, zp_b = ch.q[st.b]
+            it.kind, it.layer, it.name, it.desc = "add", None, st.name, "add"
+            it.a, it.b = t[st.a], t[st.b]
+            it.out = t[st.dst] = torch.empty_like(it.a)
+            it.args = (s_a, zp_a, s_b, zp_b, st.s_o, st.zp_o, st.act)
+            it.macs, it.bytes = 0, 3 * it.a.numel()
+            it.run = (lambda it=it: Q.add(it.a, it.args[0], it.args[1], it.b, it.args[2], it.args[3], it.args[4],
+                                          it.args[5], "i8", it.args[6], out=it.out))
+        items.append(it)
+    return items, N
+
+
 def setup(workload):
     import torch
     from paper_2006_10226_amd import qnn as Q
 
+    if workload == "resnet50_b32_chain":
+        return setup_chain(32)
     layers, batch = _layers(workload)
     items = []
     for kind, layer, c in layers:
@@ -211,7 +256,12 @@ def cpu_baseline(workload, target_s=12.0):
     from oracle import oracle as O
     import workloads as W
 
-    layers, _ = _layers(workload)
+    if workload == "resnet50_b32_chain":
+        # the chain's conv shapes, sampled on independent seeded inputs
+        layers, _ = _layers("resnet50_b32")
+        layers = [(k, l, c) for k, l, c in layers if not l.name.startswith("stem")]
+    else:
+        layers, _ = _layers(workload)
     convs = [(k, l, c) for k, l, c in layers if k in ("conv", "dense", "dw")]
 
     def run(per_layer):

@@ -1387,6 +1387,20 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
     args.zpb = b_q.zero_point[0];
     args.zp_y = y_q.zero_point[0];
     args.rounding = rounding;
+    // 24-bit product form of the rounding (8-bit operands, ties up, shifts
+    // in [17, 40], nonzero multipliers)
+    args.fast = rounding == QNN_ROUND_HALF_UP && args.ma > 0 && args.mb > 0 && args.na >= 17 && args.na <= 40 &&
+                args.nb >= 17 && args.nb <= 40;
+    if (args.fast) {
+        args.mah = args.ma >> 16;
+        args.mal = args.ma & 0xffff;
+        args.npa = args.na - 16;
+        args.ca = 1 << (args.npa - 1);
+        args.mbh = args.mb >> 16;
+        args.mbl = args.mb & 0xffff;
+        args.npb = args.nb - 16;
+        args.cb = 1 << (args.npb - 1);
+    }
     const bool aligned = (((uintptr_t)a | (uintptr_t)b | (uintptr_t)y) & 15) == 0;
     const hipError_t e = launch_add(args, a_dtype, b_dtype, y_dtype, aligned, (hipStream_t)stream);
     return e == hipSuccess ? QNN_OK : hip_fail(e, "add launch");

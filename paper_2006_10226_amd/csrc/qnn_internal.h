@@ -151,6 +151,11 @@ struct AddArgs {
     int64_t count;
     int32_t ma, na, zpa, mb, nb, zpb, zp_y;
     int32_t lo, hi, rounding;
+    // HALF_UP with both shifts in [17, 40]: each operand's rounding from two
+    // 24-bit products (multiplier halves mh = mult >> 16, ml = mult & 0xffff,
+    // np = shift - 16, c = 2^(np - 1)); the operands are 8-bit, so the
+    // zero-point-adjusted values fit 9 bits
+    int32_t fast, mah, mal, npa, ca, mbh, mbl, npb, cb;
 };
 
 // Tile configurations of the MFMA conv kernel.

@@ -100,3 +100,19 @@ def test_requantize_two_stage_ties(yt):
         assert_equal(y, ref, f"two-stage ties {s_in}/{s_out}")
         differs += int((ref != O.requantize(x, s_in, 0, s_out, 0, yt, None, "half_up")).sum())
     assert differs > 1000
+
+
+@pytest.mark.parametrize("ratio", [2.0**13 * 1.5, 2.0**-10 * 1.5, 2.0**14 * 1.5, 2.0**-11 * 1.5, 0.62, 1.0])
+def test_add_shift_range(ratio):
+    """Input / output scale ratios whose fixed-point shifts sit at the edges
+    of the 24-bit product form of the add (shifts 17 and 40) and just
+    outside it (16 and 41: the 64-bit form), for every pair of input bytes."""
+    a = np.repeat(np.arange(256, dtype=np.int32), 256).astype(np.uint8)
+    b = np.tile(np.arange(256, dtype=np.int32), 256).astype(np.uint8)
+    s_o = 0.01
+    s_a = float(np.float32(ratio * s_o))
+    s_b = float(np.float32(0.37 * s_o))
+    for rounding in ("half_up", "half_away"):
+        y = Q.add(dev(a), s_a, 131, dev(b), s_b, 7, s_o, -5, "i8", None, rounding).cpu().numpy()
+        ref = O.add(a, s_a, 131, b, s_b, 7, s_o, -5, "i8", None, rounding)
+        assert_equal(y, ref, f"add ratio {ratio} {rounding}")
