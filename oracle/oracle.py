@@ -52,6 +52,8 @@ def _load():
     lib.oracle_round_mul_shift.restype = i64
     lib.oracle_requantize_value.argtypes = [i64, f64, i32, i32, i64, i64, i32, P]
     lib.oracle_requantize_value.restype = ctypes.c_int
+    lib.oracle_pool2d.argtypes = [P, i32, P, P, i32, i32, i32, i32, P]
+    lib.oracle_pool2d.restype = ctypes.c_int
     lib.oracle_conv_out_hw.argtypes = [P, P, P, P]
     lib.oracle_conv_out_hw.restype = None
     lib.oracle_conv2d_acc.argtypes = [P, i32, i32, P, P, P, P, P, i32, P]
@@ -304,4 +306,32 @@ def add(a, s_a, zp_a, b, s_b, zp_b, s_o, zp_o, yt="u8", act=None, rounding="half
                             DTYPE_CODE[np.dtype(NAME_TO_NP[yt])], lo, hi, ROUNDING[rounding], _ptr(y))
     if rc != 0:
         raise ValueError("invalid add multipliers")
+    return y
+
+
+POOL_MODES = {"avg": 0, "max": 1}
+
+
+def pool2d(x, mode="avg", kernel=(3, 3), stride=(1, 1), pads=(0, 0, 0, 0), count_pad=False, zp=0,
+           rounding="half_away"):
+    """Quantized pool2d, Eq. (4): scale and zero point pass through, the
+    quantized input is pooled.  x NHWC u8/i8; pads (top, left, bottom, right);
+    "avg" rounds sum / count to nearest (ties by ``rounding``: "half_up" or
+    "half_away"), counting padded cells as ``zp`` when ``count_pad``; "max"
+    takes the largest in-input cell.  Returns the NHWC output, x's dtype."""
+    if rounding not in ("half_up", "half_away"):
+        raise ValueError("pool2d rounding is half_up or half_away")
+    x = np.ascontiguousarray(x)
+    N, H, W, C = x.shape
+    R, S = kernel
+    sh, sw = stride
+    pt, pl, pb, pr = pads
+    Ho, Wo = (H + pt + pb - R) // sh + 1, (W + pl + pr - S) // sw + 1
+    y = np.zeros((N, max(Ho, 0), max(Wo, 0), C), dtype=x.dtype)
+    shape = np.array([N, H, W, C, R, S], np.int32)
+    pp = np.array([sh, sw, pt, pl, pb, pr], np.int32)
+    rc = _load().oracle_pool2d(_ptr(x), DTYPE_CODE[x.dtype], _ptr(shape), _ptr(pp), POOL_MODES[mode],
+                               int(bool(count_pad)), int(zp), ROUNDING[rounding], _ptr(y))
+    if rc != 0:
+        raise ValueError("pool2d: a window holds no input cell")
     return y

@@ -36,6 +36,15 @@
  *     half-up rounding.
  *   - qnn.add: each input is requantized to the output scale (without its
  *     own output zero point), the two are added, then zp_out and the clamp.
+ *   - Quantized pooling, Eq. (4): input and output share one scale and
+ *     zero point, so the quantized output is the pooled quantized input.
+ *     Average: the sum of the window's cells (wide integers, no overflow)
+ *     divided by the cell count and rounded to the nearest integer, ties by
+ *     the selected rounding (HALF_UP or HALF_AWAY; the paper asks for care
+ *     with this rounding but does not fix it).  Cells outside the input are
+ *     either left out of sum and count, or counted with the zero point as
+ *     their value (a real zero).  Max: the largest in-input cell (scale > 0
+ *     makes max commute with dequantization).
  *
  * Parity pins (checked by the CPU test suite, not by this file): exact
  * rational dequantize identity of Eq. (1)/(2), the four-term expansion of
@@ -455,6 +464,71 @@ int oracle_add(const void *a, int32_t at, float s_a, int32_t zp_a,
 
 /* Requantize of a single zero-point adjusted value v with real multiplier M
  * (exported for the exact-rational tests). */
+/* floor(a / b) for b > 0. */
+static int64_t floor_div(int64_t a, int64_t b)
+{
+    return a >= 0 ? a / b : -((-a + b - 1) / b);
+}
+
+/* The integer nearest to sum / count (count > 0), ties toward +infinity
+ * (HALF_UP) or away from zero (HALF_AWAY): floor((2*sum + count) / (2*count)),
+ * with the magnitude rounded and the sign restored for HALF_AWAY. */
+static int64_t round_div(int64_t sum, int64_t count, int rounding)
+{
+    if (rounding == ORACLE_HALF_AWAY) {
+        const int64_t m = floor_div(2 * (sum < 0 ? -sum : sum) + count, 2 * count);
+        return sum < 0 ? -m : m;
+    }
+    return floor_div(2 * sum + count, 2 * count);
+}
+
+/*
+ * Quantized pool2d, Eq. (4).  shape = N,H,W,C,R,S; pp = stride_h, stride_w,
+ * pad_top, pad_left, pad_bottom, pad_right; mode 0 average, 1 max;
+ * count_pad 1 counts padded cells as holding zp.  x and y are NHWC of dtype
+ * xt; Ho = (H + pt + pb - R) / stride_h + 1, likewise Wo.  Returns -1 when a
+ * window holds no cell of the input.
+ */
+int oracle_pool2d(const void *x, int32_t xt, const int32_t *shape, const int32_t *pp, int32_t mode,
+                  int32_t count_pad, int32_t zp, int32_t rounding, void *y)
+{
+    const int64_t N = shape[0], H = shape[1], W = shape[2], C = shape[3], R = shape[4], S = shape[5];
+    const int64_t sh = pp[0], sw = pp[1], pt = pp[2], pl = pp[3], pb = pp[4], pr = pp[5];
+    const int64_t Ho = (H + pt + pb - R) / sh + 1, Wo = (W + pl + pr - S) / sw + 1;
+    int bad = 0;
+#pragma omp parallel for collapse(2) reduction(| : bad)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t oh = 0; oh < Ho; ++oh)
+            for (int64_t ow = 0; ow < Wo; ++ow)
+                for (int64_t c = 0; c < C; ++c) {
+                    int64_t sum = 0, count = 0, best = 0, seen = 0;
+                    for (int64_t r = 0; r < R; ++r)
+                        for (int64_t t = 0; t < S; ++t) {
+                            const int64_t h = oh * sh - pt + r, w = ow * sw - pl + t;
+                            if (h < 0 || h >= H || w < 0 || w >= W) {
+                                if (count_pad) {
+                                    sum += zp;
+                                    ++count;
+                                }
+                                continue;
+                            }
+                            const int64_t v = q_load(x, xt, ((n * H + h) * W + w) * C + c);
+                            sum += v;
+                            ++count;
+                            if (!seen || v > best)
+                                best = v;
+                            seen = 1;
+                        }
+                    if (!seen) {
+                        bad = 1;
+                        continue;
+                    }
+                    q_store(y, xt, ((n * Ho + oh) * Wo + ow) * C + c,
+                            mode == 1 ? best : round_div(sum, count, rounding));
+                }
+    return bad ? -1 : 0;
+}
+
 int oracle_requantize_value(int64_t v, double M, int32_t zp_out, int32_t yt,
                             int64_t lo, int64_t hi, int32_t rounding, int64_t *out)
 {
