@@ -205,6 +205,36 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
                    void *y, qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act,
                    qnn_rounding rounding);
 
+typedef enum {
+    QNN_POOL_AVG = 0,
+    QNN_POOL_MAX = 1
+} qnn_pool_mode;
+
+/*
+ * Quantized 2-D pooling, Eq. (4) (Sec. III-B, QNN pooling): input and output
+ * share one scale and zero point, so the quantized output is the pooled
+ * quantized input and no scale is involved.
+ *   x: device NHWC [N][H][W][C], UINT8 or INT8; y: device NHWC
+ *      [N][Ho][Wo][C] of the same dtype, Ho = (H + pad_top + pad_bottom -
+ *      R)/stride_h + 1, Wo likewise.
+ *   pool: strides >= 1, dilations 1, pads with 0 <= pad_top, pad_bottom < R
+ *      and 0 <= pad_left, pad_right < S (so that every window holds a cell
+ *      of the input); R*S <= 65536.
+ *   mode QNN_POOL_AVG: y = the window sum (exact, int32) divided by its cell
+ *      count, rounded to nearest with ties by `rounding` (HALF_UP or
+ *      HALF_AWAY; TWO_STAGE is rejected).  count_pad 0 leaves padded cells
+ *      out of sum and count; count_pad 1 counts them as holding zero_point
+ *      (a real zero), which must then lie in the dtype's range.
+ *   mode QNN_POOL_MAX: y = the largest cell of the window inside the input;
+ *      count_pad, zero_point and rounding are ignored.
+ * N may be 0 (then x and y may be NULL).  Tensors of 2^31 or more elements
+ * return QNN_ERR_UNSUPPORTED.  Enqueued on `stream`, no synchronization.
+ */
+qnn_status qnn_pool2d(void *stream, const void *x, qnn_dtype dtype, int32_t N, int32_t H,
+                      int32_t W, int32_t C, int32_t R, int32_t S, qnn_conv_params pool,
+                      qnn_pool_mode mode, int32_t count_pad, int32_t zero_point, void *y,
+                      qnn_rounding rounding);
+
 /* ---------------------------------------------------------------- plans */
 
 /*

@@ -11,7 +11,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libqnn.so")
 SOURCES = ["qnn_api.cpp", "conv_mfma.hip", "conv_tap.hip", "conv_dma.hip", "conv_wave.hip", "conv_halo.hip", "conv_window.hip", "elementwise.hip",
-           "depthwise.hip"]
+           "depthwise.hip", "pool.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

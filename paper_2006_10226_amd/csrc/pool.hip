@@ -1,0 +1,146 @@
+// Quantized 2-D pooling, Eq. (4) (Sec. III-B, QNN pooling): the input and
+// output share one scale and zero point, so the kernel pools the quantized
+// values directly and no requantize follows.
+//
+// Average: the window's cells are summed in int32 (the paper upcasts to
+// int16 for its targets; int32 is exact for any window of up to 2^16 cells)
+// and divided by the cell count with round to nearest, ties toward +inf
+// (HALF_UP) or away from zero (HALF_AWAY).  Max: the largest in-input cell.
+//
+// One thread takes V consecutive channels (16, 4 or 1 bytes) of one output
+// pixel; neighbouring threads take neighbouring channel groups, so each
+// window cell is one coalesced row segment.  The kernel is bound by HBM
+// traffic: every input byte once for non-overlapping windows (overlapping
+// ones re-read from L2), every output byte once.
+#include "qnn_internal.h"
+
+namespace qnn {
+
+// floor(num / den) for 0 <= num < 2^26 and 1 <= den <= 2^17 whose quotient is
+// below 512: the float estimate is within 2^-14 of the quotient, so its
+// truncation is off by at most one, which the exact integer remainder fixes.
+__device__ __forceinline__ int pool_div(int num, int den, float rcp)
+{
+    int q = (int)((float)num * rcp);
+    const int r = num - q * den;
+    q += (r >= den) - (r < 0);
+    return q;
+}
+
+template <int V>
+__device__ __forceinline__ void pool_load(const int8_t *p, unsigned (&w)[(V + 3) / 4])
+{
+    if constexpr (V == 16) {
+        const uint4 u = *(const uint4 *)p;
+        w[0] = u.x; w[1] = u.y; w[2] = u.z; w[3] = u.w;
+    } else if constexpr (V == 4) {
+        w[0] = *(const unsigned *)p;
+    } else {
+        w[0] = (unsigned char)*p;
+    }
+}
+
+template <bool SIGNED, bool MAX, int V>
+__global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
+{
+    constexpr int NW = (V + 3) / 4;
+    const unsigned groups = (unsigned)(a.C / V);
+    const long long total = (long long)a.N * a.Ho * a.Wo * groups;
+    const long long step = (long long)gridDim.x * blockDim.x;
+    for (long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x; gid < total; gid += step) {
+        const unsigned u = (unsigned)gid;
+        const unsigned g = u % groups;
+        unsigned p = u / groups;
+        const int ow = (int)(p % (unsigned)a.Wo);
+        p /= (unsigned)a.Wo;
+        const int oh = (int)(p % (unsigned)a.Ho);
+        const int n = (int)(p / (unsigned)a.Ho);
+        const int h0 = oh * a.sh - a.pt, w0 = ow * a.sw - a.pl;
+        const int r0 = max(0, -h0), r1 = min(a.R, a.H - h0);
+        const int s0 = max(0, -w0), s1 = min(a.S, a.W - w0);
+        int acc[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i)
+            acc[i] = MAX ? (SIGNED ? -128 : 0) : 0;
+        const int8_t *base = (const int8_t *)a.x + (size_t)n * a.H * a.W * a.C + (size_t)g * V;
+        for (int r = r0; r < r1; ++r) {
+            const int8_t *row = base + ((size_t)(h0 + r) * a.W + (w0 + s0)) * a.C;
+            for (int s = s0; s < s1; ++s, row += a.C) {
+                unsigned w[NW];
+                pool_load<V>(row, w);
+#pragma unroll
+                for (int i = 0; i < V; ++i) {
+                    const unsigned b = (w[i / 4] >> (8 * (i % 4))) & 0xffu;
+                    const int v = SIGNED ? (int)(signed char)b : (int)b;
+                    acc[i] = MAX ? max(acc[i], v) : acc[i] + v;
+                }
+            }
+        }
+        if constexpr (!MAX) {
+            int cnt = (r1 - r0) * (s1 - s0);
+            int pad_sum = 0;
+            if (a.count_pad) {
+                pad_sum = (a.R * a.S - cnt) * a.zp;
+                cnt = a.R * a.S;
+            }
+            const int den = 2 * cnt;
+            const float rcp = 1.0f / (float)den;
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const int sum = acc[i] + pad_sum;
+                if (a.rounding == 1) {
+                    const int m = pool_div(2 * abs(sum) + cnt, den, rcp);
+                    acc[i] = sum < 0 ? -m : m;
+                } else {
+                    // sum >= -128 * cnt, so the shifted numerator is positive
+                    const int off = SIGNED ? 128 : 0;
+                    acc[i] = pool_div(2 * sum + cnt + off * den, den, rcp) - off;
+                }
+            }
+        }
+        unsigned o[NW];
+#pragma unroll
+        for (int k = 0; k < NW; ++k)
+            o[k] = 0;
+#pragma unroll
+        for (int i = 0; i < V; ++i)
+            o[i / 4] |= ((unsigned)acc[i] & 0xffu) << (8 * (i % 4));
+        int8_t *dst = (int8_t *)a.y + (size_t)u * V;
+        if constexpr (V == 16)
+            *(uint4 *)dst = make_uint4(o[0], o[1], o[2], o[3]);
+        else if constexpr (V == 4)
+            *(unsigned *)dst = o[0];
+        else
+            *dst = (int8_t)(o[0] & 0xffu);
+    }
+}
+
+template <bool SIGNED, bool MAX>
+static void launch_pool_t(const PoolArgs &a, int vec, dim3 grid, hipStream_t s)
+{
+    if (vec == 16) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 16>), grid, dim3(256), 0, s, a);
+    else if (vec == 4) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 4>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 1>), grid, dim3(256), 0, s, a);
+}
+
+hipError_t launch_pool(const PoolArgs &a, bool is_signed, int vec, hipStream_t s)
+{
+    const long long threads = (long long)a.N * a.Ho * a.Wo * (a.C / vec);
+    if (threads == 0)
+        return hipSuccess;
+    long long blocks = (threads + 255) / 256;
+    const long long cap = 256LL * 32;
+    if (blocks > cap) blocks = cap;
+    const dim3 grid((unsigned)blocks);
+    const bool mx = a.mode == 1;
+    if (is_signed) {
+        if (mx) launch_pool_t<true, true>(a, vec, grid, s);
+        else launch_pool_t<true, false>(a, vec, grid, s);
+    } else {
+        if (mx) launch_pool_t<false, true>(a, vec, grid, s);
+        else launch_pool_t<false, false>(a, vec, grid, s);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace qnn

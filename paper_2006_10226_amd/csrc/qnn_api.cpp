@@ -1347,6 +1347,58 @@ qnn_status qnn_requantize(void *stream, const void *x, qnn_dtype x_dtype, int64_
     return s;
 }
 
+qnn_status qnn_pool2d(void *stream, const void *x, qnn_dtype dtype, int32_t N, int32_t H, int32_t W, int32_t C,
+                      int32_t R, int32_t S, qnn_conv_params pool, qnn_pool_mode mode, int32_t count_pad,
+                      int32_t zero_point, void *y, qnn_rounding rounding)
+{
+    if (dtype != QNN_UINT8 && dtype != QNN_INT8)
+        return fail(QNN_ERR_DTYPE, "pool2d: dtype must be uint8 or int8");
+    if (mode != QNN_POOL_AVG && mode != QNN_POOL_MAX)
+        return fail(QNN_ERR_UNSUPPORTED, "pool2d: unknown mode %d", (int)mode);
+    const bool avg = mode == QNN_POOL_AVG;
+    if (avg && rounding != QNN_ROUND_HALF_UP && rounding != QNN_ROUND_HALF_AWAY)
+        return fail(QNN_ERR_QPARAM, "pool2d: average pooling rounds HALF_UP or HALF_AWAY (got %d)", (int)rounding);
+    if (avg && count_pad != 0 && count_pad != 1)
+        return fail(QNN_ERR_SHAPE, "pool2d: count_pad must be 0 or 1");
+    const bool sgn = dtype == QNN_INT8;
+    if (avg && count_pad && (zero_point < (sgn ? -128 : 0) || zero_point > (sgn ? 127 : 255)))
+        return fail(QNN_ERR_QPARAM, "pool2d: zero point %d outside the %s range", zero_point, dtype_name(dtype));
+    if (N < 0 || H < 1 || W < 1 || C < 1 || R < 1 || S < 1)
+        return fail(QNN_ERR_SHAPE, "pool2d: sizes must be positive (N >= 0)");
+    if (pool.stride_h < 1 || pool.stride_w < 1 || pool.dil_h != 1 || pool.dil_w != 1)
+        return fail(QNN_ERR_SHAPE, "pool2d: strides must be >= 1 and dilations 1");
+    if (pool.pad_top < 0 || pool.pad_bottom < 0 || pool.pad_left < 0 || pool.pad_right < 0 ||
+        pool.pad_top >= R || pool.pad_bottom >= R || pool.pad_left >= S || pool.pad_right >= S)
+        return fail(QNN_ERR_SHAPE, "pool2d: pads must lie in [0, window size) so every window holds an input cell");
+    if ((long long)H + pool.pad_top + pool.pad_bottom < R || (long long)W + pool.pad_left + pool.pad_right < S)
+        return fail(QNN_ERR_SHAPE, "pool2d: window larger than the padded input");
+    if ((long long)R * S > 65536)
+        return fail(QNN_ERR_UNSUPPORTED, "pool2d: windows of more than 65536 cells are not supported");
+    const int Ho = (H + pool.pad_top + pool.pad_bottom - R) / pool.stride_h + 1;
+    const int Wo = (W + pool.pad_left + pool.pad_right - S) / pool.stride_w + 1;
+    if ((long long)N * H * W * C >= (1LL << 31) || (long long)N * Ho * Wo * C >= (1LL << 31))
+        return fail(QNN_ERR_UNSUPPORTED, "pool2d: tensors of 2^31 or more elements are not supported");
+    if (N == 0)
+        return QNN_OK;
+    if (!x || !y)
+        return fail(QNN_ERR_NULL, "pool2d: x or y is NULL");
+    const uintptr_t ax = (uintptr_t)x, ay = (uintptr_t)y;
+    const int vec = (C % 16 == 0 && ax % 16 == 0 && ay % 16 == 0) ? 16
+                    : (C % 4 == 0 && ax % 4 == 0 && ay % 4 == 0) ? 4 : 1;
+    PoolArgs a{};
+    a.x = x;
+    a.y = y;
+    a.N = N; a.H = H; a.W = W; a.C = C; a.R = R; a.S = S;
+    a.sh = pool.stride_h; a.sw = pool.stride_w; a.pt = pool.pad_top; a.pl = pool.pad_left;
+    a.Ho = Ho; a.Wo = Wo;
+    a.mode = avg ? 0 : 1;
+    a.count_pad = avg ? count_pad : 0;
+    a.zp = a.count_pad ? zero_point : 0;
+    a.rounding = rounding == QNN_ROUND_HALF_AWAY ? 1 : 0;
+    const hipError_t e = launch_pool(a, sgn, vec, (hipStream_t)stream);
+    return e == hipSuccess ? QNN_OK : hip_fail(e, "pool2d launch");
+}
+
 qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a_q, const void *b,
                    qnn_dtype b_dtype, qnn_qparams b_q, int64_t count, void *y, qnn_dtype y_dtype,
                    qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding)

@@ -304,4 +304,16 @@ hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, h
 hipError_t launch_cache_sweep(const void *buf, size_t bytes, int *sink, hipStream_t st);
 hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned, hipStream_t st);
 
+// Quantized pool2d (Eq. (4)): NHWC input and output of one dtype; mode 0
+// average (rounding 0 HALF_UP, 1 HALF_AWAY; count_pad counts padded cells
+// as zp), mode 1 max.  vec is 16, 4 or 1 channels per thread (C a multiple
+// of vec, x and y aligned to vec bytes).
+struct PoolArgs {
+    const void *x;
+    void *y;
+    int N, H, W, C, R, S, sh, sw, pt, pl, Ho, Wo;
+    int mode, count_pad, zp, rounding;
+};
+hipError_t launch_pool(const PoolArgs &a, bool is_signed, int vec, hipStream_t st);
+
 }  // namespace qnn

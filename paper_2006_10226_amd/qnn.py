@@ -37,6 +37,7 @@ STATUS = ["QNN_OK", "QNN_ERR_NULL", "QNN_ERR_SHAPE", "QNN_ERR_DTYPE", "QNN_ERR_Q
 EXPORTS = [
     "qnn_abi_version", "qnn_last_error", "qnn_status_string", "qnn_quantize_multiplier",
     "qnn_conv2d", "qnn_depthwise_conv2d", "qnn_dense", "qnn_requantize", "qnn_add",
+    "qnn_pool2d",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
     "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_workspace_size",
     "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
@@ -97,6 +98,8 @@ def lib() -> ctypes.CDLL:
     L.qnn_requantize.restype = st
     L.qnn_add.argtypes = [P, P, st, QParams, P, st, QParams, i64, P, st, QParams, Clamp, st]
     L.qnn_add.restype = st
+    L.qnn_pool2d.argtypes = [P, P, st, i32, i32, i32, i32, i32, i32, ConvParams, st, i32, i32, P, st]
+    L.qnn_pool2d.restype = st
     PP = ctypes.POINTER(ctypes.c_void_p)
     L.qnn_conv2d_plan_create.argtypes = [PP, P, st, i32, i32, i32, i32, QParams, P, i32, i32, i32,
                                          QParams, P, ConvParams, st, QParams, Clamp, st, i32, i32]
@@ -438,4 +441,32 @@ def add(a: torch.Tensor, a_scale, a_zp, b: torch.Tensor, b_scale, b_zp, y_scale,
     aq, bq, yq = _Q(a_scale, a_zp, 1), _Q(b_scale, b_zp, 1), _Q(y_scale, y_zp, 1)
     _check(lib().qnn_add(_stream(stream), _ptr(a), _dt(a), aq.q, _ptr(b), _dt(b), bq.q, a.numel(), _ptr(out), ydt,
                          yq.q, _clamp(act), _ROUND[rounding]))
+    return out
+
+
+_POOL_MODE = {"avg": 0, "max": 1}
+
+
+def pool2d(x: torch.Tensor, mode="avg", kernel=(3, 3), stride=(1, 1), pads=0, count_pad=False, zp=0,
+           rounding="half_away", out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Quantized pool2d of Eq. (4): NHWC u8/i8 in, same dtype out, scale and
+    zero point unchanged.  "avg" rounds sum / count to nearest (ties by
+    ``rounding``, "half_up" or "half_away"; padded cells count as ``zp`` when
+    ``count_pad``), "max" takes the largest in-input cell.  Enqueued on the
+    stream, no synchronization."""
+    _contig(x, "x")
+    if x.dim() != 4:
+        raise ValueError("pool2d input must be NHWC")
+    N, H, W, C = x.shape
+    R, S = (kernel, kernel) if isinstance(kernel, int) else kernel
+    cp = _cp(stride, pads, 1)
+    Ho = (H + cp.pad_top + cp.pad_bottom - R) // cp.stride_h + 1
+    Wo = (W + cp.pad_left + cp.pad_right - S) // cp.stride_w + 1
+    if out is None:
+        out = torch.empty((N, max(Ho, 0), max(Wo, 0), C), dtype=x.dtype, device=x.device)
+    _contig(out, "out")
+    if out.dtype != x.dtype or tuple(out.shape) != (N, Ho, Wo, C):
+        raise ValueError(f"pool2d out must be {x.dtype} of shape {(N, Ho, Wo, C)}")
+    _check(lib().qnn_pool2d(_stream(stream), _ptr(x), _dt(x), N, H, W, C, R, S, cp, _POOL_MODE[mode],
+                            int(bool(count_pad)), int(zp), _ptr(out), _ROUND[rounding]))
     return out
