@@ -18,11 +18,12 @@ namespace qnn {
 
 // floor(num / den) for 0 <= num < 2^26 and 1 <= den <= 2^17 whose quotient is
 // below 512: the float estimate is within 2^-14 of the quotient, so its
-// truncation is off by at most one, which the exact integer remainder fixes.
+// truncation is off by at most one, which the exact integer remainder fixes
+// (q * den < 2^27 is exact in the full-rate 24-bit multiply).
 __device__ __forceinline__ int pool_div(int num, int den, float rcp)
 {
     int q = (int)((float)num * rcp);
-    const int r = num - q * den;
+    const int r = num - (int)__umul24((unsigned)q, (unsigned)den);
     q += (r >= den) - (r < 0);
     return q;
 }
@@ -65,6 +66,8 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
         const int8_t *base = (const int8_t *)a.x + (size_t)n * a.H * a.W * a.C + (size_t)g * V;
         for (int r = r0; r < r1; ++r) {
             const int8_t *row = base + ((size_t)(h0 + r) * a.W + (w0 + s0)) * a.C;
+            // unrolled so that several cells' loads are in flight at once
+#pragma unroll 4
             for (int s = s0; s < s1; ++s, row += a.C) {
                 unsigned w[NW];
                 pool_load<V>(row, w);
@@ -88,13 +91,15 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
 #pragma unroll
             for (int i = 0; i < V; ++i) {
                 const int sum = acc[i] + pad_sum;
-                if (a.rounding == 1) {
+                if (!SIGNED) {
+                    // sum >= 0: both roundings agree
+                    acc[i] = pool_div(2 * sum + cnt, den, rcp);
+                } else if (a.rounding == 1) {
                     const int m = pool_div(2 * abs(sum) + cnt, den, rcp);
                     acc[i] = sum < 0 ? -m : m;
                 } else {
                     // sum >= -128 * cnt, so the shifted numerator is positive
-                    const int off = SIGNED ? 128 : 0;
-                    acc[i] = pool_div(2 * sum + cnt + off * den, den, rcp) - off;
+                    acc[i] = pool_div(2 * sum + cnt + 128 * den, den, rcp) - 128;
                 }
             }
         }

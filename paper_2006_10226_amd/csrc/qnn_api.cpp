@@ -1383,8 +1383,13 @@ qnn_status qnn_pool2d(void *stream, const void *x, qnn_dtype dtype, int32_t N, i
     if (!x || !y)
         return fail(QNN_ERR_NULL, "pool2d: x or y is NULL");
     const uintptr_t ax = (uintptr_t)x, ay = (uintptr_t)y;
-    const int vec = (C % 16 == 0 && ax % 16 == 0 && ay % 16 == 0) ? 16
-                    : (C % 4 == 0 && ax % 4 == 0 && ay % 4 == 0) ? 4 : 1;
+    int vec = (C % 16 == 0 && ax % 16 == 0 && ay % 16 == 0) ? 16
+              : (C % 4 == 0 && ax % 4 == 0 && ay % 4 == 0) ? 4 : 1;
+    // few output pixels with large windows (global pooling): fewer channels
+    // per thread so that the chip holds enough threads
+    const long long pix = (long long)N * Ho * Wo;
+    while (vec > 1 && pix * (C / vec) < 65536)
+        vec /= 4;
     PoolArgs a{};
     a.x = x;
     a.y = y;
