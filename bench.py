@@ -14,9 +14,10 @@ dominant kernel, and the CPU oracle timed on a bounded sample.
 Other workloads (--workload): mobilenet_v2_b64, inception_v3_b64, dense_bert,
 conv14x14x64 -- the same measurement on those layer sets (depthwise layers
 and adds are reported in GB/s in the per-layer file); resnet50_b32_chain --
-the 16 bottleneck blocks chained as in the network (each conv reads the int8
-tensor its producer wrote, a qnn.add closes every block; 52 convs and 16 adds,
-the stem left out), TOP/s over the convs' MACs and the whole chain's time.
+ResNet-50's conv body chained as in the network (each step reads the int8
+tensor its producer wrote: the stem, its max pool, the 16 bottleneck blocks
+with a qnn.add closing each, the global average pool; 53 convs, 16 adds, 2
+pools), TOP/s over the convs' MACs and the whole chain's time.
 """
 import argparse
 import json
@@ -89,8 +90,8 @@ class Item:
 
 
 def setup_chain(N):
-    """Plans and device tensors of the chained bottleneck blocks: every step
-    writes its own output tensor, which its consumers read."""
+    """Plans and device tensors of the chained ResNet-50 conv body: every
+    step writes its own output tensor, which its consumers read."""
     import torch
     import workloads as W
     from paper_2006_10226_amd import qnn as Q
@@ -114,6 +115,13 @@ def setup_chain(N):
             it.macs = Nb * Ho * Wo * K * L.R * L.S * L.Cin
             it.bytes = it.x.numel() + st.w.size + it.out.numel()
             it.run = (lambda it=it: it.plan.run(it.x, it.out))
+        elif isinstance(st, W.ChainPool):
+            it.kind, it.layer, it.name, it.desc = "pool", None, st.name, "pool"
+            it.x = t[st.src]
+            it.args = (st.mode, st.kernel, st.stride, st.pads)
+            it.out = t[st.dst] = Q.pool2d(it.x, *it.args)
+            it.macs, it.bytes = 0, it.x.numel() + it.out.numel()
+            it.run = (lambda it=it: Q.pool2d(it.x, *it.args, out=it.out))
         else:
             s_a, zp_a = ch.q[st.a]
             s_b, zp_b = ch.q[st.b]
@@ -177,8 +185,8 @@ def setup(workload):
 
 def kernel_group(it):
     """Kernel instantiation a layer runs (tile shape and gather width)."""
-    if it.kind == "add":
-        return "add"
+    if it.kind in ("add", "pool"):
+        return it.kind
     if it.kind == "dw":
         return "depthwise"
     words = it.desc.split()
@@ -259,7 +267,6 @@ def cpu_baseline(workload, target_s=12.0):
     if workload == "resnet50_b32_chain":
         # the chain's conv shapes, sampled on independent seeded inputs
         layers, _ = _layers("resnet50_b32")
-        layers = [(k, l, c) for k, l, c in layers if not l.name.startswith("stem")]
     else:
         layers, _ = _layers(workload)
     convs = [(k, l, c) for k, l, c in layers if k in ("conv", "dense", "dw")]

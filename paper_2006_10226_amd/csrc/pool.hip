@@ -120,6 +120,112 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
     }
 }
 
+// Few output pixels with large windows (global pooling): a workgroup of
+// SPLIT_WAVES waves takes one output pixel and 64*V channels; wave k sums
+// the window's cells k, k + SPLIT_WAVES, ... and the partial results meet
+// in LDS, where wave 0 finishes them.  Every thread reaches the barrier.
+constexpr int SPLIT_WAVES = 8;
+
+template <bool SIGNED, bool MAX, int V>
+__global__ void __launch_bounds__(64 * SPLIT_WAVES) pool_split_kernel(PoolArgs a, int chunks)
+{
+    __shared__ int part[SPLIT_WAVES][64 * V];
+    const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+    const int chunk = blockIdx.x % chunks;
+    const int p = blockIdx.x / chunks;
+    const int ow = p % a.Wo, oh = (p / a.Wo) % a.Ho, n = p / (a.Wo * a.Ho);
+    const int c0 = (chunk * 64 + lane) * V;
+    const bool active = c0 < a.C;
+    const int h0 = oh * a.sh - a.pt, w0 = ow * a.sw - a.pl;
+    const int r0 = max(0, -h0), r1 = min(a.R, a.H - h0);
+    const int s0 = max(0, -w0), s1 = min(a.S, a.W - w0);
+    const int ws = s1 - s0, cells = (r1 - r0) * ws;
+    int acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+        acc[i] = MAX ? (SIGNED ? -128 : 0) : 0;
+    if (active) {
+        const int8_t *base = (const int8_t *)a.x + (size_t)n * a.H * a.W * a.C + c0;
+#pragma unroll 4
+        for (int idx = wave; idx < cells; idx += SPLIT_WAVES) {
+            const int h = h0 + r0 + idx / ws, w = w0 + s0 + idx % ws;
+            unsigned wd[(V + 3) / 4];
+            pool_load<V>(base + ((size_t)h * a.W + w) * a.C, wd);
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const unsigned b = (wd[i / 4] >> (8 * (i % 4))) & 0xffu;
+                const int v = SIGNED ? (int)(signed char)b : (int)b;
+                acc[i] = MAX ? max(acc[i], v) : acc[i] + v;
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+        part[wave][lane * V + i] = acc[i];
+    __syncthreads();
+    if (wave != 0 || !active)
+        return;
+#pragma unroll
+    for (int k = 1; k < SPLIT_WAVES; ++k)
+#pragma unroll
+        for (int i = 0; i < V; ++i)
+            acc[i] = MAX ? max(acc[i], part[k][lane * V + i]) : acc[i] + part[k][lane * V + i];
+    if constexpr (!MAX) {
+        int cnt = cells, pad_sum = 0;
+        if (a.count_pad) {
+            pad_sum = (a.R * a.S - cnt) * a.zp;
+            cnt = a.R * a.S;
+        }
+        const int den = 2 * cnt;
+        const float rcp = 1.0f / (float)den;
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int sum = acc[i] + pad_sum;
+            if (!SIGNED) {
+                acc[i] = pool_div(2 * sum + cnt, den, rcp);
+            } else if (a.rounding == 1) {
+                const int m = pool_div(2 * abs(sum) + cnt, den, rcp);
+                acc[i] = sum < 0 ? -m : m;
+            } else {
+                acc[i] = pool_div(2 * sum + cnt + 128 * den, den, rcp) - 128;
+            }
+        }
+    }
+    int8_t *dst = (int8_t *)a.y + (size_t)p * a.C + c0;
+    unsigned o = 0;
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+        o |= ((unsigned)acc[i] & 0xffu) << (8 * i);
+    if constexpr (V == 4)
+        *(unsigned *)dst = o;
+    else
+        *dst = (int8_t)(o & 0xffu);
+}
+
+template <bool SIGNED, bool MAX>
+static void launch_split_t(const PoolArgs &a, int vec, hipStream_t s)
+{
+    const int chunks = (a.C / vec + 63) / 64;
+    const dim3 grid((unsigned)((long long)a.N * a.Ho * a.Wo * chunks));
+    if (vec == 4) hipLaunchKernelGGL((pool_split_kernel<SIGNED, MAX, 4>), grid, dim3(64 * SPLIT_WAVES), 0, s, a, chunks);
+    else hipLaunchKernelGGL((pool_split_kernel<SIGNED, MAX, 1>), grid, dim3(64 * SPLIT_WAVES), 0, s, a, chunks);
+}
+
+hipError_t launch_pool_split(const PoolArgs &a, bool is_signed, int vec, hipStream_t s)
+{
+    if ((long long)a.N * a.Ho * a.Wo == 0)
+        return hipSuccess;
+    const bool mx = a.mode == 1;
+    if (is_signed) {
+        if (mx) launch_split_t<true, true>(a, vec, s);
+        else launch_split_t<true, false>(a, vec, s);
+    } else {
+        if (mx) launch_split_t<false, true>(a, vec, s);
+        else launch_split_t<false, false>(a, vec, s);
+    }
+    return hipGetLastError();
+}
+
 template <bool SIGNED, bool MAX>
 static void launch_pool_t(const PoolArgs &a, int vec, dim3 grid, hipStream_t s)
 {

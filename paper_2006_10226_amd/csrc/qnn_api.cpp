@@ -1385,10 +1385,14 @@ qnn_status qnn_pool2d(void *stream, const void *x, qnn_dtype dtype, int32_t N, i
     const uintptr_t ax = (uintptr_t)x, ay = (uintptr_t)y;
     int vec = (C % 16 == 0 && ax % 16 == 0 && ay % 16 == 0) ? 16
               : (C % 4 == 0 && ax % 4 == 0 && ay % 4 == 0) ? 4 : 1;
-    // few output pixels with large windows (global pooling): fewer channels
-    // per thread so that the chip holds enough threads
+    // few output pixels (global pooling): with windows of 8 or more cells,
+    // several waves share each pixel's window; otherwise fewer channels per
+    // thread, so that the chip holds enough threads
     const long long pix = (long long)N * Ho * Wo;
-    while (vec > 1 && pix * (C / vec) < 65536)
+    const bool split = pix * (C / vec) < 65536 && R * S >= 8 && pix * ((C + 255) / 256) < (1LL << 31);
+    if (split)
+        vec = vec >= 4 ? 4 : 1;
+    while (!split && vec > 1 && pix * (C / vec) < 65536)
         vec /= 4;
     PoolArgs a{};
     a.x = x;
@@ -1400,7 +1404,8 @@ qnn_status qnn_pool2d(void *stream, const void *x, qnn_dtype dtype, int32_t N, i
     a.count_pad = avg ? count_pad : 0;
     a.zp = a.count_pad ? zero_point : 0;
     a.rounding = rounding == QNN_ROUND_HALF_AWAY ? 1 : 0;
-    const hipError_t e = launch_pool(a, sgn, vec, (hipStream_t)stream);
+    const hipError_t e = split ? launch_pool_split(a, sgn, vec, (hipStream_t)stream)
+                               : launch_pool(a, sgn, vec, (hipStream_t)stream);
     return e == hipSuccess ? QNN_OK : hip_fail(e, "pool2d launch");
 }
 

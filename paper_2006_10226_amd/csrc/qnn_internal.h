@@ -315,5 +315,8 @@ struct PoolArgs {
     int mode, count_pad, zp, rounding;
 };
 hipError_t launch_pool(const PoolArgs &a, bool is_signed, int vec, hipStream_t st);
+// The window-split form for few output pixels with large windows: one
+// workgroup per output pixel and 64*vec channels (vec 4 or 1).
+hipError_t launch_pool_split(const PoolArgs &a, bool is_signed, int vec, hipStream_t st);
 
 }  // namespace qnn

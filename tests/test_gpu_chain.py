@@ -1,7 +1,7 @@
-"""The 16 ResNet-50 bottleneck blocks chained as in the network (int8
-hand-off between layers, qnn.add closing every block) on the GPU against the
-oracle running the same chain on its own tensors: every one of the 68
-intermediate tensors byte for byte."""
+"""ResNet-50's conv body chained as in the network (stem, max pool, the 16
+bottleneck blocks with int8 hand-off and a qnn.add closing every block,
+global average pool) on the GPU against the oracle running the same chain on
+its own tensors: every one of the 71 intermediate tensors byte for byte."""
 import numpy as np
 import pytest
 import torch
@@ -32,6 +32,8 @@ def run_chain_gpu(ch):
             torch.cuda.synchronize()
             p.close()
             t[st.dst] = out
+        elif isinstance(st, W.ChainPool):
+            t[st.dst] = Q.pool2d(t[st.src], st.mode, st.kernel, st.stride, st.pads)
         else:
             s_a, zp_a = ch.q[st.a]
             s_b, zp_b = ch.q[st.b]
@@ -48,6 +50,8 @@ def run_chain_oracle(ch):
             L = st.layer
             t[st.dst] = O.conv2d(t[st.src], s_x, zp_x, st.w, st.s_w, st.zp_w, st.bias, st.s_y, st.zp_y, "i8",
                                  st.act, "half_up", stride=(L.stride, L.stride), pads=L.pads)
+        elif isinstance(st, W.ChainPool):
+            t[st.dst] = O.pool2d(t[st.src], st.mode, st.kernel, st.stride, st.pads)
         else:
             s_a, zp_a = ch.q[st.a]
             s_b, zp_b = ch.q[st.b]
@@ -56,14 +60,15 @@ def run_chain_oracle(ch):
 
 
 @pytest.mark.parametrize("N", [1, 2])
-def test_resnet50_bottleneck_chain(N):
+def test_resnet50_chain(N):
     ch = W.resnet50_chain(N)
     log(f"chain N={N}: {len(ch.steps)} steps")
     gpu = run_chain_gpu(ch)
     ref = run_chain_oracle(ch)
     for st in ch.steps:
         assert_equal(gpu[st.dst], ref[st.dst], f"chain N={N} {st.dst}")
+    assert len(ch.steps) == 71 and ch.steps[-1].dst == "gap" and ref["gap"].shape == (N, 1, 1, 2048)
     # the data stays informative through the chain: the last block output
-    # is neither constant nor all on the clamp
-    last = ref[ch.steps[-1].dst]
-    assert len(np.unique(last)) > 50
+    # and the pooled features are neither constant nor all on the clamp
+    assert len(np.unique(ref[ch.steps[-2].dst])) > 50
+    assert len(np.unique(ref["gap"])) > 20

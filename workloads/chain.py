@@ -1,12 +1,15 @@
-"""The 16 ResNet-50 bottleneck blocks chained as in the network: every conv
-reads the int8 tensor its producer wrote, with the producer's (scale, zero
-point), and every block ends in a qnn.add of its main path and its shortcut
-(the block input, or the projection conv of the first block of a stage).
+"""ResNet-50's conv body chained as in the network: the 7x7/2 stem, its 3x3/2
+max pool, the 16 bottleneck blocks and the global 7x7 average pool.  Every
+step reads the int8 tensor its producer wrote, with the producer's (scale,
+zero point), every block ends in a qnn.add of its main path and its shortcut
+(the block input, or the projection conv of the first block of a stage), and
+pooling keeps its input's (scale, zero point) (Eq. (4)).
 Only shapes and quantization parameters are drawn here; this module holds no
 quantized-operator arithmetic.
 
 Recipe (numpy.random.default_rng(seed), drawn in the order below):
-  * input x0: int8 uniform over [-128, 127], scale 0.02, zero point -10;
+  * input x0: an int8 image N x 224 x 224 x 3, uniform over [-128, 127],
+    scale 0.02, zero point -10;
   * per conv, in layer order: weights rint(normal(0, 30)) clipped to
     [-127, 127], per-channel scales log-uniform over one decade centred on
     48 / sigma_acc (so that an output scale stays near its input's through
@@ -18,8 +21,9 @@ Recipe (numpy.random.default_rng(seed), drawn in the order below):
     output steps): s_y = s_x * geomean(s_w) * sigma_acc / 48;
   * zero points: -100 for outputs followed by a ReLU (the clamp keeps
     [-100, 127]), 0 for the linear 1x1b and projection outputs;
-  * add: output scale 1.5 x the larger input scale, zero point -100, ReLU.
-The stem (and the max pool after it) is not part of the chain.
+  * add: output scale 1.5 x the larger input scale, zero point -100, ReLU;
+  * pools: max 3x3/2 with pads 1 after the stem, average 7x7 (rounding half
+    away from zero) after the last block.
 """
 from __future__ import annotations
 
@@ -57,10 +61,21 @@ class ChainAdd:
 
 
 @dataclass
+class ChainPool:
+    name: str
+    src: str
+    dst: str
+    mode: str                            # "max" or "avg"
+    kernel: Tuple[int, int]
+    stride: Tuple[int, int]
+    pads: Tuple[int, int, int, int]
+
+
+@dataclass
 class Chain:
-    x0: np.ndarray                       # int8 NHWC input of the first block
+    x0: np.ndarray                       # int8 NHWC image
     q: dict                              # tensor name -> (scale, zero point)
-    steps: List[Union[ChainConv, ChainAdd]]
+    steps: List[Union[ChainConv, ChainAdd, ChainPool]]
     N: int
 
 
@@ -70,11 +85,12 @@ def _f32(v) -> float:
 
 def resnet50_chain(N: int, seed: int = 6000) -> Chain:
     rng = np.random.default_rng(seed)
+    stem = [l for l in resnet50() if l.name.startswith("stem")][0]
     layers = [l for l in resnet50() if not l.name.startswith("stem")]
-    x0 = rng.integers(-128, 128, size=(N, 56, 56, 64), dtype=np.int8)
+    x0 = rng.integers(-128, 128, size=(N, 224, 224, 3), dtype=np.int8)
     q = {"x0": (0.02, -10)}
     spread2 = {"x0": float(np.mean((x0.astype(np.float64) + 10.0) ** 2))}
-    steps: List[Union[ChainConv, ChainAdd]] = []
+    steps: List[Union[ChainConv, ChainAdd, ChainPool]] = []
 
     def conv(layer: ConvLayer, src: str, dst: str):
         s_x, _ = q[src]
@@ -93,7 +109,14 @@ def resnet50_chain(N: int, seed: int = 6000) -> Chain:
         steps.append(ChainConv(layer, src, dst, w, s_w, np.zeros(layer.Cout, np.int32), bias, s_y, zp_y,
                                (zp_y, 127) if relu else None))
 
-    cur = "x0"
+    def pool(name, src, dst, mode, kernel, stride, pads):
+        q[dst] = q[src]
+        spread2[dst] = spread2[src]
+        steps.append(ChainPool(name, src, dst, mode, kernel, stride, pads))
+
+    conv(stem, "x0", "stem")
+    pool("stem_pool", "stem", "pool", "max", (3, 3), (2, 2), (1, 1, 1, 1))
+    cur = "pool"
     i = 0
     while i < len(layers):
         pre = layers[i].name.split("_")[0]
@@ -112,4 +135,5 @@ def resnet50_chain(N: int, seed: int = 6000) -> Chain:
         steps.append(ChainAdd(pre + "_add", pre + "_c", short, pre + "_out", s_o, -100, (-100, 127)))
         cur = pre + "_out"
         i += len(block)
+    pool("gap", cur, "gap", "avg", (7, 7), (1, 1), (0, 0, 0, 0))
     return Chain(x0, q, steps, N)
