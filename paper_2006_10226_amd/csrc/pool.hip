@@ -41,7 +41,11 @@ __device__ __forceinline__ void pool_load(const int8_t *p, unsigned (&w)[(V + 3)
     }
 }
 
-template <bool SIGNED, bool MAX, int V>
+// PACK (average, V >= 4, windows of at most 257 cells): bytes 0 and 2 of
+// each loaded word are summed in the two 16-bit halves of one register,
+// bytes 1 and 3 in another (int8 biased by +128 first); 257 * 255 < 2^16,
+// so no half carries into the other.
+template <bool SIGNED, bool MAX, int V, bool PACK = false>
 __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
 {
     constexpr int NW = (V + 3) / 4;
@@ -64,6 +68,10 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
         for (int i = 0; i < V; ++i)
             acc[i] = MAX ? (SIGNED ? -128 : 0) : 0;
         const int8_t *base = (const int8_t *)a.x + (size_t)n * a.H * a.W * a.C + (size_t)g * V;
+        unsigned even[NW], odd[NW];
+#pragma unroll
+        for (int k = 0; k < NW; ++k)
+            even[k] = odd[k] = 0;
         for (int r = r0; r < r1; ++r) {
             const int8_t *row = base + ((size_t)(h0 + r) * a.W + (w0 + s0)) * a.C;
             // unrolled so that several cells' loads are in flight at once
@@ -71,12 +79,29 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
             for (int s = s0; s < s1; ++s, row += a.C) {
                 unsigned w[NW];
                 pool_load<V>(row, w);
+                if constexpr (PACK) {
 #pragma unroll
-                for (int i = 0; i < V; ++i) {
-                    const unsigned b = (w[i / 4] >> (8 * (i % 4))) & 0xffu;
-                    const int v = SIGNED ? (int)(signed char)b : (int)b;
-                    acc[i] = MAX ? max(acc[i], v) : acc[i] + v;
+                    for (int k = 0; k < NW; ++k) {
+                        const unsigned x = SIGNED ? w[k] ^ 0x80808080u : w[k];
+                        even[k] += x & 0x00ff00ffu;
+                        odd[k] += (x >> 8) & 0x00ff00ffu;
+                    }
+                } else {
+#pragma unroll
+                    for (int i = 0; i < V; ++i) {
+                        const unsigned b = (w[i / 4] >> (8 * (i % 4))) & 0xffu;
+                        const int v = SIGNED ? (int)(signed char)b : (int)b;
+                        acc[i] = MAX ? max(acc[i], v) : acc[i] + v;
+                    }
                 }
+            }
+        }
+        if constexpr (PACK) {
+            const int bias = SIGNED ? 128 * (r1 - r0) * (s1 - s0) : 0;
+#pragma unroll
+            for (int i = 0; i < V; ++i) {
+                const unsigned h = (i % 2 == 0 ? even[i / 4] : odd[i / 4]) >> (16 * ((i % 4) / 2));
+                acc[i] = (int)(h & 0xffffu) - bias;
             }
         }
         if constexpr (!MAX) {
@@ -229,7 +254,10 @@ hipError_t launch_pool_split(const PoolArgs &a, bool is_signed, int vec, hipStre
 template <bool SIGNED, bool MAX>
 static void launch_pool_t(const PoolArgs &a, int vec, dim3 grid, hipStream_t s)
 {
-    if (vec == 16) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 16>), grid, dim3(256), 0, s, a);
+    const bool pack = !MAX && (long long)a.R * a.S <= 257;
+    if (vec == 16 && pack) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 16, !MAX>), grid, dim3(256), 0, s, a);
+    else if (vec == 16) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 16>), grid, dim3(256), 0, s, a);
+    else if (vec == 4 && pack) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 4, !MAX>), grid, dim3(256), 0, s, a);
     else if (vec == 4) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 4>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 1>), grid, dim3(256), 0, s, a);
 }

@@ -122,3 +122,23 @@ def test_rejected_arguments():
     with pytest.raises(Q.QnnError):
         Q.pool2d(x, "avg", (9, 3), (1, 1), 0)                     # window larger than the input
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dt", ["u8", "i8"])
+def test_packed_sum_window_bounds(dt):
+    # windows of 257 cells (the largest whose byte sums the kernel packs two
+    # to a register: 257 * 255 = 65535) and of 272 cells (summed unpacked),
+    # on outputs large enough for the one-pixel-per-thread kernel
+    rng = np.random.default_rng(7500)
+    hi = O.DTYPE_RANGE[dt][1]
+    for (N, H, W, R, S) in ((6, 64, 300, 1, 257), (28, 40, 40, 16, 17)):
+        for fill in ("max", "random"):
+            if fill == "max":
+                x = np.full((N, H, W, 64), hi, O.NAME_TO_NP[dt])
+            else:
+                x = _rand(rng, (N, H, W, 64), dt)
+            for rounding in ("half_up", "half_away"):
+                tag = f"{dt} {R}x{S} {fill} {rounding}"
+                log(f"pool {tag}")
+                got = _run(x, "avg", (R, S), (1, 1), (0, 0, 0, 0), rounding=rounding)
+                assert_equal(got, O.pool2d(x, "avg", (R, S), (1, 1), (0, 0, 0, 0), rounding=rounding), tag)
