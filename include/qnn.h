@@ -153,6 +153,11 @@ qnn_status qnn_conv2d(void *stream,
 /*
  * Depthwise conv2d with channel multiplier 1 + bias + requantize + clamp:
  * acc[n,oh,ow,c] = sum_{r,s} (x~[.., c] - zp_x)(w[r][s][c] - zp_w[c]) + bias[c].
+ * This is Eq. (2) with each output channel reading only its own input
+ * channel (so J = R*S), evaluated in the subtract-first form that Sec.
+ * III-B gives as the alternative lowering of the QNN convolution; x~ is x
+ * inside the image and zp_x in the padding (Sec. III-B); the requantize is
+ * Eq. (5).
  *   w: device int8 [R][S][C]; w_q per tensor or per channel (n == C).
  *   y: NHWC [N][Ho][Wo][C] with row stride y_ldc >= y_coff + C.
  * Other arguments as qnn_conv2d.  Synchronizes `stream` before returning.
@@ -168,6 +173,10 @@ qnn_status qnn_depthwise_conv2d(void *stream,
 /*
  * qnn.dense + bias + requantize + clamp:
  * acc[m,j] = sum_k (x[m,k] - zp_x)(w[j,k] - zp_w[j]) + bias[j].
+ * Sec. III-D names matrix multiplication beside conv2d as the operators
+ * whose integer schedules need data reuse; its accumulator is Eq. (2)/(3)
+ * with a 1x1 window over Kd input channels (the four terms of Eq. (3) with
+ * J = Kd), followed by the requantize of Eq. (5).
  *   x: device [M][Kd] (UINT8/INT8), w: device int8 [Nd][Kd], bias [Nd] or NULL,
  *   y: device [M][y_ldc] with y_ldc >= Nd.  Synchronizes `stream`.
  */
@@ -197,6 +206,13 @@ qnn_status qnn_requantize(void *stream, const void *x, qnn_dtype x_dtype, int64_
 /*
  * qnn.add of two same-shape tensors with different per-tensor qparams:
  *   y = clamp(zp_y + round((a - zp_a) * s_a / s_y) + round((b - zp_b) * s_b / s_y))
+ * A quantized add is named among the operators a framework adds (Sec. I-B)
+ * but its lowering is not given; this follows the paper's principle that a
+ * quantized operator decomposes into simpler existing ones (Sec. II-B, and
+ * Sec. III-A: QNN operators are wrappers around sequences of them): each
+ * input is requantized to the output scale by Eq. (5) without its zero
+ * point, the two integers are added, then zp_y is added and the result
+ * clamped.
  * a, b: device UINT8/INT8 arrays of `count` elements; y: UINT8/INT8.
  * Enqueued on `stream`, no synchronization.
  */

@@ -648,7 +648,10 @@ int device_cus()
     return cus;
 }
 
-qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
+// tune: time the candidate kernels when the kernel-choice records hold no
+// choice for this shape (plans); one-shot calls pass false and take the
+// recorded choice or else the first candidate, without timing.
+qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, bool tune = true)
 {
     int32_t Ho, Wo, lo, hi;
     std::vector<int32_t> mult, shift;
@@ -802,6 +805,11 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     if (rowpack && (int64_t)d.N * Hp * Wp * C4 >= (int64_t(1) << 31)) {
         free_plan(p);
         return fail(QNN_ERR_UNSUPPORTED, "padded image of 2^31 bytes or more");
+    }
+    // the kernels index the channel-padded copy (C4 channels) in int32
+    if (!rowpack && C4 != d.C && (int64_t)d.N * d.H * d.W * C4 >= (int64_t(1) << 31)) {
+        free_plan(p);
+        return fail(QNN_ERR_UNSUPPORTED, "channel-padded input of 2^31 bytes or more");
     }
     const bool dma_ok = tap_ok && border_classes(d, Ho, Wo, M, bc);
     const bool pcorr = dma_ok && bc.any && zpx != 0;
@@ -992,7 +1000,7 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out)
     ConvKernel best = cands[0];
     if (cands.size() > 1 && M > 0 && env_int("QNN_AUTOTUNE", 1) != 0) {
         const std::string key = tune_key(d, term3, ncls, fast);
-        if (!tune_lookup(key, cands, &best)) {
+        if (!tune_lookup(key, cands, &best) && tune) {
             if ((s = autotune_conv(a, cands, p->avec, term3, pcorr_tab, pcls_tab, st, &best)) != QNN_OK) {
                 free_plan(p);
                 return s;
@@ -1146,7 +1154,7 @@ qnn_status one_shot(const ConvDesc &d, hipStream_t st, const void *x, void *y)
             return s;
     }
     qnn_plan *p = nullptr;
-    qnn_status s = make_conv_plan(d, st, &p);
+    qnn_status s = make_conv_plan(d, st, &p, false);
     if (s != QNN_OK)
         return s;
     if ((s = alloc_ws(p)) == QNN_OK && (s = run_plan(p, st, x, y, nullptr)) == QNN_OK) {

@@ -108,6 +108,8 @@ def _conv(Q, **kw):
     (dict(ys=1e-13), "QNN_ERR_QPARAM"),          # multiplier >= 2^30
     (dict(C=4096, R=3, S=3, xz=0, wz=[127]), "QNN_ERR_OVERFLOW"),   # 36864 * 255 * 255 >= 2^31
     (dict(N=2**20, H=64, W=64), "QNN_ERR_UNSUPPORTED"),
+    # 9 channels padded to 12 for the gather: N*H*W*9 < 2^31 <= N*H*W*12
+    (dict(H=14000, W=14000, C=9, K=4, y_ldc=4), "QNN_ERR_UNSUPPORTED"),
 ])
 def test_conv_validation_errors(Q, kw, expect):
     st, msg = _conv(Q, **kw)
