@@ -172,7 +172,7 @@ def setup(workload):
             it.plan, it.w, it.bias = plan, w, bias
             it.x = torch.from_numpy(c.x).cuda()
             it.out = plan.new_output()
-            it.ws = (torch.empty(plan.workspace_size, dtype=torch.uint8, device="cuda")
+            it.ws = (torch.zeros(plan.workspace_size, dtype=torch.uint8, device="cuda")
                      if plan.workspace_size else None)
             it.desc = plan.describe()
             it.macs = _macs(kind, layer, c, plan.out_shape)

@@ -90,7 +90,7 @@ constexpr int dma_occupancy()
 // stages); the second group's partial sums are added through LDS before
 // the first group's epilogue.  For tiles too few to fill the chip this
 // puts two waves on each SIMD and twice the MFMA work behind each barrier.
-template <int TC, int TP, int WC, int WP, int NS, bool FLIP, bool SHORT, int KS = 1>
+template <int TC, int TP, int WC, int WP, int NS, bool FLIP, bool SHORT, int KS = 1, bool SPLIT = false>
 __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<TC / WC, TP / WP>()))
     conv_dma_kernel(ConvArgs a)
 {
@@ -110,6 +110,7 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
     static_assert(KS == 1 || (!SHORT && NW * FC * FP * 1024 <= LDS_BYTES), "split groups: ring form, partials fit");
     static_assert(LPS * (SHORT ? NS - 1 : NSG - 2) < 64, "vmcnt range");
     static_assert(SHORT || NSG >= 4, "the fragment prefetch needs stage k + 1 to land one step early");
+    static_assert(!SPLIT || (!SHORT && KS == 1), "split reductions: ring form, one K-step group");
 
     __shared__ __attribute__((aligned(1024))) int8_t lds[LDS_BYTES];
     // the tile's channel records, fetched at the start for the epilogue
@@ -123,12 +124,22 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
     const int wc = wave / WP, wpos = wave % WP;
 
     // XCD x (workgroups dealt round-robin) takes the x-th eighth of the
-    // tile list; consecutive tiles are the channel tiles of one pixel tile.
-    const int chunk = (a.ntiles + 7) >> 3;
+    // work list; consecutive tiles are the channel tiles of one pixel tile.
+    // Split reduction (a.ksplit = S > 1, ring form): a work unit is one of
+    // the S parts of a tile's K-steps, and the S parts of a tile are
+    // consecutive units, so they run on one XCD at the same time.
+    const int S = SPLIT ? a.ksplit : 1;
+    const int units = a.ntiles * S;
+    const int chunk = (units + 7) >> 3;
     const int xcd = blockIdx.x & 7;
-    const int tile = xcd * chunk + (blockIdx.x >> 3);
-    if (tile >= min(a.ntiles, (xcd + 1) * chunk))
+    const int unit = xcd * chunk + (blockIdx.x >> 3);
+    if (unit >= min(units, (xcd + 1) * chunk))
         return;
+    const int tile = SPLIT ? unit / S : unit;
+    const int part = SPLIT ? unit - tile * S : 0;
+    // this unit's K-steps: [kbeg, kbeg + nk)
+    const int kbeg = SPLIT ? (int)((long long)part * a.nk / S) : 0;
+    const int nk = SPLIT ? (int)((long long)(part + 1) * a.nk / S) - kbeg : a.nk;
     const int c0 = (tile % a.tiles_c) * TC;
     const int p0 = (tile / a.tiles_c) * TP;
 
@@ -195,7 +206,6 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
     }
 
     // ---- loader: tap (lr, ls) and channel offset lc of the next stage ---
-    const int nk = a.nk;
     int lr = 0, ls = 0, lc = 0;
     int voffB[LB];
     auto set_tap = [&]() {
@@ -207,17 +217,30 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
             voffB[i] = v ? pbase[i] + toff : kOutOfRange;
         }
     };
-    // one K-step of the loader: channel slice, then tap
+    // one K-step of the loader: channel slice, then tap; steps past the end
+    // of the unit's reduction are cut by the liveness test of issue()
+    int wk = kbeg;   // K-step whose weights the next issue loads
     auto advance = [&]() {
+        ++wk;
         lc += BK;
         if (lc == a.C) {
             lc = 0;
             if (++ls == a.S) {
                 ls = 0;
-                ++lr;   // lr == R past the last tap: every row reads out of range
+                if (++lr == a.R)
+                    lr = 0;
             }
             set_tap();
         }
+    };
+    // loader position of K-step k0 (C % 64 == 0: whole taps of C / 64 steps)
+    auto start_at = [&](int k0) {
+        wk = k0;
+        const int cpt = a.C / BK;
+        const int t = k0 / cpt;
+        lc = (k0 - t * cpt) * BK;
+        lr = t / a.S;
+        ls = t - lr * a.S;
     };
     // LDS buffer of a group's local stage ks (global K-step ks * KS + grp)
     auto stage_buf = [&](int ks) { return lds + ((ks & (NSG - 1)) * KS + grp) * STAGE; };
@@ -228,15 +251,15 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
         int8_t *base = stage_buf(ks);
         const int gs = ks * KS + grp;
         const bool live = gs < nk;
-        const int soffA = __builtin_amdgcn_readfirstlane(live ? gs * BK : 0);
-        const int oobA = __builtin_amdgcn_readfirstlane(live ? 0 : kOutOfRange);
+        const int soffA = __builtin_amdgcn_readfirstlane(live ? (a.rowpack ? gs : wk) * BK : 0);
+        const int oob = __builtin_amdgcn_readfirstlane(live ? 0 : kOutOfRange);
         const int soffB = __builtin_amdgcn_readfirstlane(lc);
 #pragma unroll
         for (int i = 0; i < LA; ++i)
-            dma16(rw, base + (i * NW + wave) * 16 * BK, voffA[i] | oobA, soffA);
+            dma16(rw, base + (i * NW + wave) * 16 * BK, voffA[i] | oob, soffA);
 #pragma unroll
         for (int i = 0; i < LB; ++i)
-            dma16(rx, base + TC * BK + (i * NW + wave) * 16 * BK, voffB[i], soffB);
+            dma16(rx, base + TC * BK + (i * NW + wave) * 16 * BK, voffB[i] | oob, soffB);
         if (a.rowpack) {
             ++lr;   // next row pair; lr == R (pairs) past the end: out of range
             set_tap();
@@ -325,6 +348,8 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
         // group grp starts at K-step grp; both groups run the same number of
         // local steps (a step past the end reads zeros), so every barrier
         // is reached by every wave
+        if (SPLIT)
+            start_at(kbeg);
         set_tap();
         for (int q = 0; q < grp; ++q)
             advance();
@@ -333,7 +358,7 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
         for (int s = 0; s < NSG - 1; ++s)
             issue(s);
         stage_barrier<LPS *(NSG - 2)>();
-        if (grp == 0)
+        if (grp == 0 && part == 0)
             add_bconst<TC, TP, WC, WP, true>(acc, recs);   // the records landed with stage 0
         read_frags(0, fa[0], fb[0]);
         constexpr std::integral_constant<int, FC + FP> kNext{};
@@ -356,6 +381,61 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
         lds_wait<0>();
         wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
         __syncthreads();
+        if constexpr (SPLIT) {
+            // Each unit stores its partial sums (int32, in the accumulator
+            // layout) and counts itself in the tile's counter; the unit that
+            // arrives last adds the other parts to its own and runs the
+            // epilogue, then resets the counter to 0 for the next launch.
+            // Integer addition is exact, so the order of the parts does not
+            // matter.  The parts of a tile may run on different XCDs, whose
+            // L2s are not coherent with each other: the partial sums are
+            // stored and loaded with agent-scope coherence (sc1: written
+            // through to, and read from, the device's coherence point, as the
+            // relaxed agent-scope atomic loads and stores of this target are),
+            // and the stores are complete (vmcnt 0) before the counter is
+            // incremented.  No cache-wide write-back or invalidate is needed.
+            constexpr int kAgentScope = 16;   // cache policy bit sc1
+            constexpr int SLOT = NW * FC * FP * 64 * 16;   // bytes of one unit's partial tile
+            __shared__ int arrived;
+            {
+                const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+                    (void *)((char *)a.part + (size_t)unit * SLOT), (short)0, SLOT, kBufFlags);
+#pragma unroll
+                for (int i = 0; i < FC; ++i)
+#pragma unroll
+                    for (int j = 0; j < FP; ++j)
+                        __builtin_amdgcn_raw_buffer_store_b128(acc[i][j], rp,
+                                                               (((wave * FC + i) * FP + j) * 64 + lane) * 16, 0,
+                                                               kAgentScope);
+            }
+            wait_vmcnt<0>();
+            __syncthreads();
+            if (tid == 0)
+                arrived = __hip_atomic_fetch_add(a.cnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __syncthreads();
+            if (arrived != S - 1)
+                return;
+            if (tid == 0)
+                __hip_atomic_store(a.cnt + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int q = 0; q < S; ++q) {
+                if (q == part)
+                    continue;
+                const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+                    (void *)((char *)a.part + ((size_t)tile * S + q) * SLOT), (short)0, SLOT, kBufFlags);
+                v4i t[FC][FP];
+#pragma unroll
+                for (int i = 0; i < FC; ++i)
+#pragma unroll
+                    for (int j = 0; j < FP; ++j)
+                        t[i][j] = __builtin_amdgcn_raw_buffer_load_b128(rq, (((wave * FC + i) * FP + j) * 64 + lane) * 16,
+                                                                       0, kAgentScope);
+#pragma unroll
+                for (int i = 0; i < FC; ++i)
+#pragma unroll
+                    for (int j = 0; j < FP; ++j)
+                        acc[i][j] += t[i][j];
+            }
+        }
         if constexpr (KS > 1) {
             // the second group's partial sums, through LDS, into the first's
             v4i *part = (v4i *)lds;
@@ -502,6 +582,19 @@ TileShape dma_tile_shape(int tile)
     return {kDmaCfg[tile].tc, kDmaCfg[tile].tp, 64};
 }
 
+// ring configurations with a split-reduction instantiation
+static constexpr bool dma_split_cfg(int t)
+{
+    return t == DMA_128x128_S4 || t == DMA_128x128_S8 || t == DMA_128x64_S4 || t == DMA_64x128_S4 ||
+           t == DMA_64x64_S4 || t == DMA_64x64_S8 || t == DMA_256x128_S4 || t == DMA_128x256_S4 ||
+           t == DMA_256x128_W4 || t == DMA_128x256_W4;
+}
+
+bool dma_splits(int tile)
+{
+    return tile >= 0 && tile < DMA_COUNT && dma_split_cfg(tile);
+}
+
 int dma_threads(int tile)
 {
     return kDmaCfg[tile].wc * kDmaCfg[tile].wp * 64 * kDmaCfg[tile].ks;
@@ -531,6 +624,22 @@ static hipError_t launch_dma_cfg(const ConvArgs &a, hipStream_t st)
         return hipErrorInvalidValue;   // more K-steps than the short form holds
     if (c.ks > 1 && a.rowpack)
         return hipErrorInvalidValue;   // the row-pair walk steps one K-step at a time
+    if (a.ksplit > 1) {
+        if constexpr (dma_split_cfg(T)) {
+            if (a.rowpack || a.C % 64 != 0 || !a.part || !a.cnt)
+                return hipErrorInvalidValue;   // split parts start at whole 64-channel steps
+            const int units = (a.ntiles * a.ksplit + 7) / 8 * 8;
+            if (a.flip4)
+                hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, false, 1, true>),
+                                   dim3(units), dim3(c.wc * c.wp * 64), 0, st, a);
+            else
+                hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, false, 1, true>),
+                                   dim3(units), dim3(c.wc * c.wp * 64), 0, st, a);
+            return hipGetLastError();
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     if (a.flip4)
         hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, c.sh, c.ks>), dim3(grid),
                            dim3(c.wc * c.wp * 64 * c.ks), 0, st, a);

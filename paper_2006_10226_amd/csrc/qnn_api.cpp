@@ -144,6 +144,7 @@ enum KernelFamily { FAM_GATHER = 0, FAM_TAP = 1, FAM_DMA = 2, FAM_WAVE = 3, FAM_
 struct ConvKernel {
     int fam = FAM_GATHER;
     int tile = TILE_64x64;
+    int split = 1;   // LDS-direct ring kernel: K-step parts per tile
 };
 
 struct qnn_plan {
@@ -154,6 +155,7 @@ struct qnn_plan {
     ConvKernel ker;             // kernel family and tile that run_plan launches
     bool term3 = false;
     size_t ws_asum_bytes = 0, ws_xpad_bytes = 0;
+    size_t ws_cnt_bytes = 0, ws_part_bytes = 0;   // split reduction: counters, partial sums
     int32_t C_in = 0;           // channels of the caller's x (before padding to a.C)
     bool rowpack = false;       // row-pair mode: x is copied into a zero-point padded image
     int32_t H_in = 0, W_in = 0, pt_in = 0, pl_in = 0;   // caller's image and pads (row-pair mode)
@@ -328,8 +330,13 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
     auto tap_fits = [&](int t) { return C4 % tap_tile_shape(t).bk == 0 || one_tap; };
     if ((f_wave == 1 || f_wave == 2 || f_wave == 4 || f_wave == 8) && wave_ok)
         return {{FAM_WAVE, f_wave}};
-    if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok && (!dma_short(f_dma) || (J + 63) / 64 <= dma_stages(f_dma)))
+    if (f_dma >= 0 && f_dma < DMA_COUNT && dma_ok && (!dma_short(f_dma) || (J + 63) / 64 <= dma_stages(f_dma))) {
+        // QNN_KSPLIT=<parts> with a forced ring configuration that has a split form
+        const int f_split = env_int("QNN_KSPLIT", 1);
+        if (f_split > 1 && dma_splits(f_dma) && C4 % 64 == 0 && J / 64 >= f_split)
+            return {{FAM_DMA, f_dma, f_split}};
         return {{FAM_DMA, f_dma}};
+    }
     if (f_tap >= 0 && f_tap < TAP_COUNT && tap_ok && tap_fits(f_tap))
         return {{FAM_TAP, f_tap}};
     if (f_tile >= 0 && f_tile < TILE_COUNT)
@@ -354,6 +361,24 @@ std::vector<ConvKernel> conv_candidates(int64_t M, int K, int C4, int J, bool ta
         for (int t = DMA_64x128_R1; t < DMA_COUNT; ++t)
             if (dma_short(t) && (J + 63) / 64 <= dma_stages(t))
                 c.push_back({FAM_DMA, t});
+        // split reductions, for grids of fewer tiles than about two per CU:
+        // each tile's K-steps in parts of at least three steps, run by
+        // separate workgroups whose partial sums the last one adds
+        if (C4 % 64 == 0 && env_int("QNN_SPLIT", 1) != 0) {
+            const int nk = J / 64;
+            const int64_t cus = device_cus();
+            for (int t = 0; t < DMA_COUNT; ++t) {
+                if (!dma_splits(t))
+                    continue;
+                const TileShape ts = dma_tile_shape(t);
+                const int64_t tiles = (int64_t)((K + ts.tc - 1) / ts.tc) * ((M + ts.tp - 1) / ts.tp);
+                if (tiles >= 2 * cus)
+                    continue;
+                for (int sp : {2, 3, 4, 6, 8, 12, 16})
+                    if (nk >= 3 * sp && tiles * sp <= 4 * cus)
+                        c.push_back({FAM_DMA, t, sp});
+            }
+        }
     }
     if (c.empty() || C4 % 64 != 0) {
         // the general gather kernel (short reductions use the 64-deep
@@ -390,6 +415,7 @@ void set_tiling(ConvArgs &a, const ConvKernel &k, int avec, const int32_t *pcorr
     a.tiles_c = (int)tiles_c;
     a.ntiles = ntiles >= 0 && ntiles < (int64_t(1) << 31) - 8 ? (int)ntiles : -1;
     a.nk = (a.J + ts.bk - 1) / ts.bk;
+    a.ksplit = k.fam == FAM_DMA ? k.split : 1;
     a.nblocks = 0;
     if (k.fam == FAM_GATHER && a.ntiles >= 0) {
         // persistent grid: as many workgroups as stay resident, a multiple
@@ -422,10 +448,20 @@ qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &ca
     const size_t elem = base.mode == OUT_INT32 ? 4 : 1;
     const size_t yb = align_up((size_t)base.M * base.y_ldc * elem, 256);
     const size_t sb = align_up((size_t)base.M * sizeof(int32_t), 256);
+    // split reductions: counters (zeroed, reset by every launch) and partial sums
+    size_t cb = 0, pb = 0;
+    for (const ConvKernel &k : cands) {
+        if (k.fam != FAM_DMA || k.split <= 1)
+            continue;
+        const TileShape ts = kernel_shape(k);
+        const size_t tiles = (size_t)((base.K + ts.tc - 1) / ts.tc) * ((base.M + ts.tp - 1) / ts.tp);
+        cb = std::max(cb, align_up(tiles * sizeof(int32_t), 256));
+        pb = std::max(pb, tiles * k.split * ts.tc * ts.tp * sizeof(int32_t));
+    }
     void *buf = nullptr;
-    hipError_t e = hipMalloc(&buf, xb + yb + sb);
+    hipError_t e = hipMalloc(&buf, xb + yb + sb + cb + pb);
     if (e != hipSuccess)
-        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes for kernel tuning failed", xb + yb + sb);
+        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes for kernel tuning failed", xb + yb + sb + cb + pb);
     // Each timed launch starts with cold caches, as a layer does inside a
     // network: a pass over more than the L2s and the 256 MB last-level cache
     // runs before it.  (Without the buffer the timing is warm.)
@@ -451,7 +487,11 @@ qnn_status autotune_conv(const ConvArgs &base, const std::vector<ConvKernel> &ca
     a.x = (const uint8_t *)buf;
     a.y = (char *)buf + xb;
     a.asum = term3 ? (const int32_t *)((char *)buf + xb + yb) : nullptr;
-    if ((e = hipMemsetAsync(buf, 0x35, xb + yb + sb, st)) != hipSuccess || (e = hipEventCreate(&e0)) != hipSuccess ||
+    a.cnt = cb ? (int32_t *)((char *)buf + xb + yb + sb) : nullptr;
+    a.part = cb ? (int32_t *)((char *)buf + xb + yb + sb + cb) : nullptr;
+    if ((e = hipMemsetAsync(buf, 0x35, xb + yb + sb, st)) != hipSuccess ||
+        (cb && (e = hipMemsetAsync((char *)buf + xb + yb + sb, 0, cb, st)) != hipSuccess) ||
+        (e = hipEventCreate(&e0)) != hipSuccess ||
         (e = hipEventCreate(&e1)) != hipSuccess) {
         s = hip_fail(e, "kernel tuning set-up");
     } else {
@@ -520,7 +560,7 @@ bool tune_lookup(const std::string &key, const std::vector<ConvKernel> &cands, C
     if (it == g_tune.end())
         return false;
     for (const ConvKernel &k : cands)
-        if (k.fam == it->second.fam && k.tile == it->second.tile) {
+        if (k.fam == it->second.fam && k.tile == it->second.tile && k.split == it->second.split) {
             *out = k;
             return true;
         }
@@ -534,7 +574,7 @@ void tune_record(const std::string &key, const ConvKernel &k)
     if (g_tune_path.empty())
         return;
     if (FILE *f = std::fopen(g_tune_path.c_str(), "a")) {
-        std::fprintf(f, "%s %d %d\n", key.c_str(), k.fam, k.tile);
+        std::fprintf(f, "%s %d %d %d\n", key.c_str(), k.fam, k.tile, k.split);
         std::fclose(f);
     }
 }
@@ -1014,6 +1054,12 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
         free_plan(p);
         return fail(QNN_ERR_UNSUPPORTED, "too many output tiles");
     }
+    if (a.ksplit > 1) {
+        const TileShape st_ = kernel_shape(best);
+        p->ws_cnt_bytes = align_up((size_t)a.ntiles * sizeof(int32_t), 256);
+        p->ws_part_bytes = (size_t)a.ntiles * a.ksplit * st_.tc * st_.tp * sizeof(int32_t);
+        p->ws_bytes += p->ws_cnt_bytes + p->ws_part_bytes;
+    }
     const TileShape ts = kernel_shape(best);
     static const char *fam_name[] = {"conv_mfma", "conv_tap", "conv_dma", "conv_wave", "conv_halo", "conv_window"};
     char buf[200];
@@ -1037,6 +1083,9 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
     if (best.fam == FAM_WAVE) {
         const size_t n = strlen(buf);
         snprintf(buf + n, sizeof buf - n, " split=%d", best.tile);
+    } else if (best.fam == FAM_DMA && best.split > 1) {
+        const size_t n = strlen(buf);
+        snprintf(buf + n, sizeof buf - n, " ksplit=%d", best.split);
     } else if (best.fam == FAM_WIN) {
         const size_t n = strlen(buf);
         snprintf(buf + n, sizeof buf - n, " cfg=%d", best.tile);
@@ -1067,6 +1116,10 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
             if (!ws)
                 return fail(QNN_ERR_NULL, "plan_run: the plan needs a workspace");
             a.asum = p->term3 ? (const int32_t *)ws : nullptr;
+            if (p->ws_cnt_bytes) {
+                a.cnt = (int32_t *)((char *)ws + p->ws_asum_bytes + p->ws_xpad_bytes);
+                a.part = (int32_t *)((char *)a.cnt + p->ws_cnt_bytes);
+            }
         }
         hipError_t e;
         if (p->ws_xpad_bytes) {
@@ -1140,6 +1193,9 @@ qnn_status alloc_ws(qnn_plan *p)
         return QNN_OK;
     if (hipMalloc(&p->ws_own, p->ws_bytes) != hipSuccess)
         return fail(QNN_ERR_ALLOC, "hipMalloc of a %zu-byte workspace failed", p->ws_bytes);
+    // split reductions need their arrival counters at zero before the first run
+    if (p->ws_cnt_bytes && hipMemset(p->ws_own, 0, p->ws_bytes) != hipSuccess)
+        return fail(QNN_ERR_HIP, "zeroing the workspace failed");
     return QNN_OK;
 }
 
@@ -1562,11 +1618,13 @@ qnn_status qnn_set_tuning_file(const char *path)
         if (!f && errno != ENOENT)
             return fail(QNN_ERR_UNSUPPORTED, "cannot read the tuning file %s: %s", path, std::strerror(errno));
         if (f) {
-            char key[256];
-            int fam = 0, tile = 0;
-            while (std::fscanf(f, "%255s %d %d", key, &fam, &tile) == 3)
-                if (fam >= FAM_GATHER && fam <= FAM_WIN && tile >= 0)
-                    rec[key] = ConvKernel{fam, tile};
+            char line[512], key[256];
+            while (std::fgets(line, sizeof line, f)) {
+                int fam = 0, tile = 0, split = 1;
+                const int n = std::sscanf(line, "%255s %d %d %d", key, &fam, &tile, &split);
+                if (n >= 3 && fam >= FAM_GATHER && fam <= FAM_WIN && tile >= 0 && split >= 1)
+                    rec[key] = ConvKernel{fam, tile, n == 4 ? split : 1};
+            }
             std::fclose(f);
         }
     }

@@ -105,6 +105,13 @@ struct ConvArgs {
     // padded image (H, W padded, pads 0), R counts filter row pairs, S is 1,
     // and row_bytes is the padded image's row stride
     int32_t rowpack, row_bytes;
+    // split reduction of the LDS-direct ring kernel: each tile's K-steps in
+    // ksplit parts run by separate workgroups; part[] holds their int32
+    // partial sums (ntiles * ksplit * TC * TP), cnt[] one arrival counter per
+    // tile (zero between launches: the last part resets it)
+    int32_t ksplit;
+    int32_t *part;
+    int32_t *cnt;
 };
 
 // Depthwise conv arguments (channel multiplier 1).
@@ -234,6 +241,7 @@ enum DmaTile {
 };
 TileShape dma_tile_shape(int tile);
 int dma_threads(int tile);
+bool dma_splits(int tile);   // the configuration has a split-reduction form
 int dma_split(int tile);    // K-step groups sharing a tile (1 or 2)
 int dma_stages(int tile);
 bool dma_short(int tile);   // short-reduction form: at most dma_stages(tile) K-steps

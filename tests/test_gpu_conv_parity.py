@@ -269,8 +269,8 @@ def test_plan_workspace_and_streams():
     assert p.workspace_size > 0, p.describe()
     x = dev(c.x)
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
-    ws1 = torch.empty(p.workspace_size, dtype=torch.uint8, device="cuda")
-    ws2 = torch.empty(p.workspace_size, dtype=torch.uint8, device="cuda")
+    ws1 = torch.zeros(p.workspace_size, dtype=torch.uint8, device="cuda")
+    ws2 = torch.zeros(p.workspace_size, dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     with torch.cuda.stream(s1):
         y1 = p.run(x, workspace=ws1, stream=s1)
