@@ -377,8 +377,12 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
             mfma(std::integral_constant<int, 0>{}, fa[0], fb[0]);
         // with an even step count the reads of step nk (past the last one)
         // are still in flight: retire them before their registers are
-        // reused (the compiler does not know they are pending)
+        // reused (the compiler does not know they are pending); the
+        // fragments stay live up to the wait, so that no instruction the
+        // compiler schedules before it can be given their registers
         lds_wait<0>();
+        lds_settled(fa[0]);
+        lds_settled(fb[0]);
         wait_vmcnt<0>();                   // the trailing out-of-range loads also write LDS
         __syncthreads();
         if constexpr (SPLIT) {
