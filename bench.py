@@ -30,6 +30,12 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+# Committed kernel choices (qnn_set_tuning_file records): the plans of these
+# workloads take them instead of timing candidates on the machine at hand,
+# so the benchmark, its profiles and the full-tensor parity test of the
+# same layers run the same kernels.
+CHOICE_FILES = {"resnet50_b32": os.path.join("workloads", "choices", "resnet50_b32.txt")}
+
 PEAK_INT8_TOPS = 5000.0   # MI355X dense int8 MFMA, TOP/s
 PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, GB/s
 METRIC = "effective int8 TOPS + % of int8 MFMA peak, qnn.conv2d+requantize"
@@ -338,7 +344,10 @@ def main():
                          "FETCH_SIZE / WRITE_SIZE counters, and exit")
     ap.add_argument("--layers-out", default=None, help="write per-layer timings as JSON to this file")
     ap.add_argument("--tuning-file", default=None,
-                    help="kernel-choice file: reuse the choices recorded there, append newly timed ones")
+                    help="kernel-choice file: reuse the choices recorded there, append newly timed ones "
+                         "(default for the ResNet-50 b32 workload: a copy of the committed choices)")
+    ap.add_argument("--retune", action="store_true",
+                    help="time the candidate kernels on this machine instead of taking the committed choices")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -357,6 +366,18 @@ def main():
         torch.cuda.synchronize()
         log(f"copied {n} bytes 3 times")
         return
+    choice = "timed on this machine"
+    if args.tuning_file is None and not args.retune and args.workload in CHOICE_FILES:
+        src = os.path.join(ROOT, CHOICE_FILES[args.workload])
+        if os.path.exists(src):
+            import shutil
+            import tempfile
+            fd, args.tuning_file = tempfile.mkstemp(prefix="qnn_choices_", suffix=".txt")
+            os.close(fd)
+            shutil.copyfile(src, args.tuning_file)   # a copy: newly timed shapes are appended to it, not to src
+            choice = CHOICE_FILES[args.workload]
+    elif args.tuning_file:
+        choice = args.tuning_file
     if args.tuning_file:
         from paper_2006_10226_amd import qnn
         qnn.set_tuning_file(args.tuning_file)
@@ -473,7 +494,7 @@ def main():
         "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic (seeded, architecture shapes only, random weights)",
-        "config": {"workload": args.workload, "batch": batch, "layers": len(items),
+        "config": {"workload": args.workload, "batch": batch, "layers": len(items), "kernel_choice": choice,
                    "gmac_per_step": round(total_macs / 1e9, 3), "launch": "hipGraph" if graphed else "eager",
                    "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4),
                    # sum over layers of max(MFMA time at peak, algorithmic bytes at HBM peak),

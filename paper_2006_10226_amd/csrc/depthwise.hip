@@ -55,7 +55,12 @@ __global__ void __launch_bounds__(256) depthwise3_kernel(DwArgs a)
     // 32-bit index arithmetic and buffer addressing throughout
     const unsigned nch = (unsigned)a.C >> 3;
     const unsigned nstrip = ((unsigned)a.Wo + P - 1) / P;
-    const unsigned gid = blockIdx.x * blockDim.x + threadIdx.x;
+    // workgroups are dealt to the 8 XCDs round-robin and each XCD has its
+    // own L2: XCD x takes the x-th eighth of the work list (the grid is a
+    // multiple of 8), so the output rows that share input rows run on one
+    // XCD and the input is fetched from HBM about once
+    const unsigned lb = (blockIdx.x & 7u) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    const unsigned gid = lb * blockDim.x + threadIdx.x;
     if (gid >= (unsigned)a.items)
         return;
     const unsigned chunk = gid % nch;
@@ -241,7 +246,7 @@ hipError_t launch_depthwise3(const DwArgs &a, hipStream_t st)
         return hipErrorInvalidValue;
     if (a.items == 0)
         return hipSuccess;
-    const dim3 grid((unsigned)((a.items + 255) / 256));
+    const dim3 grid((unsigned)(((a.items + 255) / 256 + 7) / 8 * 8));
     if (a.sw == 1)
         a.zpw_any ? launch_dw3_out<1, true>(a, grid, st) : launch_dw3_out<1, false>(a, grid, st);
     else
