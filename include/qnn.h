@@ -306,7 +306,27 @@ qnn_status qnn_requantize_plan_create(qnn_plan **plan, void *stream,
 qnn_status qnn_plan_run(const qnn_plan *plan, void *stream, const void *x, void *y,
                         void *workspace);
 
-/* Bytes of device workspace a run needs (0 if none). */
+/*
+ * Allocation-free run, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): runs the plan like qnn_plan_run, with its workspace taken from
+ * a static device array of the library (64 MiB per device: 1 MiB of
+ * counters, 63 MiB for the rest), held by each GPU the library runs on
+ * until the process ends.  x and y are the caller's device buffers as in
+ * qnn_plan_run.  Allocates nothing and does not synchronize; the first
+ * call on a device also clears the counter region with a kernel on
+ * `stream` and must not be under stream capture (QNN_ERR_UNSUPPORTED).
+ * A plan whose workspace exceeds the array returns QNN_ERR_UNSUPPORTED
+ * with nothing enqueued.  Every call on one device shares the array:
+ * calls that overlap on one GPU (two streams, two threads) race, so such
+ * callers must order them or use qnn_plan_run with separate workspaces.
+ */
+qnn_status qnn_plan_run_noalloc(const qnn_plan *plan, void *stream, const void *x, void *y);
+
+/* Bytes of device workspace a run needs (0 if none).  When the plan uses a
+ * split reduction its workspace starts with arrival counters, which must be
+ * zero before the first run with that workspace; every run leaves them
+ * zero (the plan's own workspace is zeroed at allocation). */
 size_t qnn_plan_workspace_size(const qnn_plan *plan);
 
 /* Human-readable kernel choice of the plan, e.g. "conv_dma tile=128x128x64

@@ -1099,7 +1099,11 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
     return QNN_OK;
 }
 
-qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *ws)
+// Runs a plan with its workspace in two parts: `cnt` holds the split
+// reduction's arrival counters (zero between runs), `ws` the window sums,
+// the padded input copy and the partial sums, in that order.  A workspace
+// of qnn_plan_workspace_size bytes holds the counters first, then the rest.
+qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *cnt, void *ws)
 {
     switch (p->kind) {
     case PLAN_CONV: {
@@ -1111,14 +1115,12 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
         a.x = (const uint8_t *)x;
         a.y = y;
         if (p->ws_bytes) {
-            if (!ws)
-                ws = p->ws_own;
-            if (!ws)
+            if (!ws || (p->ws_cnt_bytes && !cnt))
                 return fail(QNN_ERR_NULL, "plan_run: the plan needs a workspace");
             a.asum = p->term3 ? (const int32_t *)ws : nullptr;
             if (p->ws_cnt_bytes) {
-                a.cnt = (int32_t *)((char *)ws + p->ws_asum_bytes + p->ws_xpad_bytes);
-                a.part = (int32_t *)((char *)a.cnt + p->ws_cnt_bytes);
+                a.cnt = (int32_t *)cnt;
+                a.part = (int32_t *)((char *)ws + p->ws_asum_bytes + p->ws_xpad_bytes);
             }
         }
         hipError_t e;
@@ -1185,6 +1187,14 @@ qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, v
     }
     }
     return fail(QNN_ERR_UNSUPPORTED, "unknown plan kind");
+}
+
+qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *ws)
+{
+    if (!ws)
+        ws = p->ws_own;
+    char *base = (char *)ws;
+    return run_plan_at(p, st, x, y, base, base ? base + p->ws_cnt_bytes : nullptr);
 }
 
 qnn_status alloc_ws(qnn_plan *p)
@@ -1313,6 +1323,62 @@ qnn_status make_req_plan(qnn_dtype xt, int64_t count, int32_t channels, qnn_qpar
              (long long)count, channels, (int)perch);
     p->desc = buf;
     *out = p;
+    return QNN_OK;
+}
+
+// ---------------------------------------------------------------- allocation-free runs
+//
+// qnn_plan_run_noalloc takes its workspace from this file-scope device
+// array instead of memory the caller or the plan allocated: the first
+// kScratchCntBytes hold the split reduction's arrival counters (zero
+// between runs: every split kernel resets the counters it used), the rest
+// the window sums, the padded input copy and the partial sums of one run.
+// In host code `scratch` names a host-side stand-in; its device address is
+// taken once per device (hipGetSymbolAddress) and only that address is
+// passed to kernels.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr size_t kScratchCntBytes = size_t(1) << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+__global__ void __launch_bounds__(256) zero_words_kernel(uint32_t *p, size_t n)
+{
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
+std::mutex g_scratch_mu;
+char *g_scratch[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device.  On the first
+// call for a device its counter region is cleared by a kernel on `st` (not
+// a memset, so that the clear is stream-ordered like the runs after it).
+qnn_status scratch_for_device(hipStream_t st, char **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(QNN_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if ((e = hipStreamIsCapturing(st, &cs)) != hipSuccess)
+            return hip_fail(e, "hipStreamIsCapturing");
+        if (cs != hipStreamCaptureStatusNone)
+            return fail(QNN_ERR_UNSUPPORTED,
+                        "plan_run_noalloc: the first call on a device sets up its scratch and must not be captured");
+        void *ptr = nullptr;
+        if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch))) != hipSuccess || !ptr)
+            return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress of the scratch array");
+        hipLaunchKernelGGL(zero_words_kernel, dim3(256), dim3(256), 0, st, (uint32_t *)ptr,
+                           kScratchCntBytes / sizeof(uint32_t));
+        if ((e = hipGetLastError()) != hipSuccess)
+            return hip_fail(e, "scratch clear launch");
+        g_scratch[dev] = (char *)ptr;
+    }
+    *out = g_scratch[dev];
     return QNN_OK;
 }
 
@@ -1604,6 +1670,25 @@ qnn_status qnn_plan_run(const qnn_plan *plan, void *stream, const void *x, void 
     if (!plan)
         return fail(QNN_ERR_NULL, "plan_run: plan is NULL");
     return run_plan(plan, (hipStream_t)stream, x, y, workspace);
+}
+
+qnn_status qnn_plan_run_noalloc(const qnn_plan *plan, void *stream, const void *x, void *y)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_run_noalloc: plan is NULL");
+    const size_t data = plan->ws_bytes - plan->ws_cnt_bytes;
+    if (plan->ws_cnt_bytes > kScratchCntBytes || data > kScratchBytes - kScratchCntBytes)
+        return fail(QNN_ERR_UNSUPPORTED,
+                    "plan_run_noalloc: the plan needs %zu bytes of counters and %zu of workspace, the static scratch "
+                    "holds %zu and %zu",
+                    plan->ws_cnt_bytes, data, kScratchCntBytes, kScratchBytes - kScratchCntBytes);
+    if (!plan->ws_bytes)
+        return run_plan_at(plan, (hipStream_t)stream, x, y, nullptr, nullptr);
+    char *sc = nullptr;
+    qnn_status s = scratch_for_device((hipStream_t)stream, &sc);
+    if (s != QNN_OK)
+        return s;
+    return run_plan_at(plan, (hipStream_t)stream, x, y, sc, sc + kScratchCntBytes);
 }
 
 size_t qnn_plan_workspace_size(const qnn_plan *plan) { return plan ? plan->ws_bytes : 0; }

@@ -39,7 +39,7 @@ EXPORTS = [
     "qnn_conv2d", "qnn_depthwise_conv2d", "qnn_dense", "qnn_requantize", "qnn_add",
     "qnn_pool2d",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
-    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_workspace_size",
+    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
     "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
 ]
 
@@ -114,6 +114,8 @@ def lib() -> ctypes.CDLL:
     L.qnn_requantize_plan_create.restype = st
     L.qnn_plan_run.argtypes = [P, P, P, P, P]
     L.qnn_plan_run.restype = st
+    L.qnn_plan_run_noalloc.argtypes = [P, P, P, P]
+    L.qnn_plan_run_noalloc.restype = st
     L.qnn_plan_workspace_size.argtypes = [P]
     L.qnn_plan_workspace_size.restype = ctypes.c_size_t
     L.qnn_plan_describe.argtypes = [P]
@@ -265,6 +267,19 @@ class Plan:
                 self.workspace_size:
             raise ValueError("workspace is smaller than the plan needs")
         _check(lib().qnn_plan_run(self._h, _stream(stream), _ptr(x), _ptr(out), _ptr(workspace)))
+        return out
+
+    def run_noalloc(self, x: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+        """qnn_plan_run_noalloc: the workspace is the library's static device
+        array; out must be given (nothing is allocated)."""
+        _contig(x, "x")
+        _contig(out, "out")
+        if tuple(x.shape) != self.in_shape or x.dtype != self.in_dtype:
+            raise ValueError(f"x is {tuple(x.shape)} {x.dtype}, the plan expects {self.in_shape} {self.in_dtype}")
+        if tuple(out.shape) != self.y_ldc_shape or out.dtype != self.out_dtype:
+            raise ValueError(f"out is {tuple(out.shape)} {out.dtype}, the plan writes {self.y_ldc_shape} "
+                             f"{self.out_dtype}")
+        _check(lib().qnn_plan_run_noalloc(self._h, _stream(stream), _ptr(x), _ptr(out)))
         return out
 
     def close(self):
