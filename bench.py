@@ -202,6 +202,8 @@ def kernel_group(it):
         extra += f" split={d['split']}"
     if "cfg" in d:
         extra += f" cfg={d['cfg']}"
+    if "ksplit" in d:
+        extra += " ksplit"
     return f"{words[0]} tile={d['tile']} {extra}"
 
 
@@ -246,20 +248,30 @@ def time_steps(items, steps, warmup, use_graph):
 
 
 def time_launches(items, steps):
-    """Per-launch kernel time: each layer's launch bracketed by events on the
-    stream it runs on (torch's current stream), over `steps` eager steps."""
+    """Per-launch kernel time over `steps` eager steps, on the stream the
+    kernels run on (torch's current stream).  A layer with a plan runs through
+    qnn_plan_run_timed, whose main kernel records the two events at its own
+    start and end (hipExtLaunchKernel): its duration as rocprofv3 reports it.
+    Other steps (adds, pools) are bracketed by events around the call, which
+    also times the dispatch gaps.  Returns (median ms per item, how)."""
     import torch
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in items]
           for _ in range(steps)]
     torch.cuda.synchronize()
     for s in range(steps):
         for i, it in enumerate(items):
-            ev[s][i][0].record()
-            it.run()
-            ev[s][i][1].record()
+            a, b = ev[s][i]
+            if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw"):
+                it.plan.run_timed(it.x, it.out, getattr(it, "ws", None), a, b)
+            else:
+                a.record()
+                it.run()
+                b.record()
     torch.cuda.synchronize()
     per = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # ms
-    return np.median(per, axis=0)
+    how = ["kernel" if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw") else "bracketed"
+           for it in items]
+    return np.median(per, axis=0), how
 
 
 # ------------------------------------------------------------------ CPU oracle baseline
@@ -310,12 +322,12 @@ def cpu_baseline(workload, target_s=12.0):
 
 # ------------------------------------------------------------------ traffic from committed counters
 
-def traffic_for(group, workload):
+def traffic_for(group, workload, layers):
     """HBM bytes per launch of the dominant kernel from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary of this workload
     (profiles/traffic_<workload>.json, or profiles/traffic.json when it
-    names the workload), if it was taken on the current kernel source (else
-    None)."""
+    names the workload), if it was taken on the current kernel source and
+    the group held the same layers there (else None)."""
     from paper_2006_10226_amd.rocprof_summary import kernel_source_sha1
     for name in (f"traffic_{workload}.json", "traffic.json"):
         path = os.path.join(ROOT, "profiles", name)
@@ -325,7 +337,10 @@ def traffic_for(group, workload):
             rec = json.load(open(path))
             if rec.get("workload") != workload or rec.get("source_sha1") != kernel_source_sha1(ROOT):
                 return None
-            return rec.get("groups", {}).get(group, {}).get("bytes_per_launch")
+            g = rec.get("groups", {}).get(group, {})
+            if sorted(g.get("layers", [])) != sorted(layers):
+                return None
+            return g.get("bytes_per_launch")
         except Exception:
             return None
     return None
@@ -398,23 +413,25 @@ def main():
     value = 2.0 * total_macs / (ms * 1e-3) / 1e12
     log(f"step {ms:.4f} ms -> {value:.1f} TOP/s (graph={graphed})")
 
-    per = time_launches(items, args.steps)
+    per, how = time_launches(items, args.steps)
     groups = {}
     for it, t in zip(items, per):
         g = kernel_group(it)
-        d = groups.setdefault(g, {"launches": 0, "ms": 0.0, "macs": 0, "bytes": 0})
+        d = groups.setdefault(g, {"launches": 0, "ms": 0.0, "macs": 0, "bytes": 0, "layers": []})
         d["launches"] += 1
         d["ms"] += float(t)
         d["macs"] += it.macs
         d["bytes"] += it.bytes
+        d["layers"].append(it.name)
     dom = max(groups, key=lambda g: groups[g]["ms"])
     D = groups[dom]
-    # Each launch bracketed by its own events also times the event packets
-    # and dispatch gaps around it (about 2 us); the graph step has none of
-    # that.  The group's share of the event-timed step, applied to the
-    # graph-timed step, gives its average kernel duration.
+    # The dominant group's average kernel duration, from the events its main
+    # kernels recorded at their own start and end (the duration rocprofv3's
+    # kernel trace reports).  The step also holds the dispatch gaps between
+    # kernels; the layers' shares of the step (for the aggregates below)
+    # spread them in proportion to the kernel times.
     scale = ms / float(np.sum(per))
-    avg_ms = D["ms"] * scale / D["launches"]
+    avg_ms = D["ms"] / D["launches"]
     # the group's bound is the lower of its two roofs: a conv or dense group
     # whose algorithmic ops per byte sit above the ridge (peak ops / peak
     # bytes) is bound by the matrix cores, below it by HBM (as depthwise,
@@ -429,11 +446,12 @@ def main():
         achieved = D["bytes"] / D["launches"] / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof["traffic"] = traffic_for(dom, args.workload)
+    roof["traffic"] = traffic_for(dom, args.workload, D["layers"])
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_ms * 1e3, 3)
-    roof["avg_launch_us_event_bracketed"] = round(D["ms"] / D["launches"] * 1e3, 3)
+    roof["avg_launch_us_step_share"] = round(avg_ms * scale * 1e3, 3)
     roof["launches_per_step"] = D["launches"]
+    roof["layers"] = D["layers"]
 
     def roofline_us(it):
         return max(2.0 * it.macs / (PEAK_INT8_TOPS * 1e12), it.bytes / (PEAK_HBM_GBS * 1e9)) * 1e6
@@ -456,8 +474,8 @@ def main():
                          "ceiling_frac_of_int8_peak": round(cb_ops / (cb_roof_us * 1e-6) / 1e12 / PEAK_INT8_TOPS, 4),
                          "share_of_step": round(cb_ms / ms, 4)}
     layer_rows = []
-    for it, t in zip(items, per):
-        row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3),
+    for it, t, h in zip(items, per, how):
+        row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3), "timed": h,
                "gmac": round(it.macs / 1e9, 4), "mbytes": round(it.bytes / 1e6, 3)}
         if it.macs:
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)

@@ -307,6 +307,18 @@ qnn_status qnn_plan_run(const qnn_plan *plan, void *stream, const void *x, void 
                         void *workspace);
 
 /*
+ * qnn_plan_run for measurement: the plan's main kernel (the conv, dense or
+ * depthwise kernel, not the auxiliary window-sum or padding kernels) is
+ * launched with hipExtLaunchKernel, which records start_event and
+ * stop_event (hipEvent_t, created by the caller, passed as void*) at that
+ * kernel's own start and end, so their elapsed time is the kernel's
+ * duration as a profiler reports it.  Nothing is recorded when the plan has
+ * no output pixels.  Requantize plans return QNN_ERR_UNSUPPORTED.
+ */
+qnn_status qnn_plan_run_timed(const qnn_plan *plan, void *stream, const void *x, void *y, void *workspace,
+                              void *start_event, void *stop_event);
+
+/*
  * Allocation-free run, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): runs the plan like qnn_plan_run, with its workspace taken from

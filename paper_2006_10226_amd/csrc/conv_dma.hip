@@ -634,10 +634,10 @@ static hipError_t launch_dma_cfg(const ConvArgs &a, hipStream_t st)
                 return hipErrorInvalidValue;   // split parts start at whole 64-channel steps
             const int units = (a.ntiles * a.ksplit + 7) / 8 * 8;
             if (a.flip4)
-                hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, false, 1, true>),
+                launch_main((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, false, 1, true>),
                                    dim3(units), dim3(c.wc * c.wp * 64), 0, st, a);
             else
-                hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, false, 1, true>),
+                launch_main((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, false, 1, true>),
                                    dim3(units), dim3(c.wc * c.wp * 64), 0, st, a);
             return hipGetLastError();
         } else {
@@ -645,10 +645,10 @@ static hipError_t launch_dma_cfg(const ConvArgs &a, hipStream_t st)
         }
     }
     if (a.flip4)
-        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, c.sh, c.ks>), dim3(grid),
+        launch_main((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, true, c.sh, c.ks>), dim3(grid),
                            dim3(c.wc * c.wp * 64 * c.ks), 0, st, a);
     else
-        hipLaunchKernelGGL((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, c.sh, c.ks>), dim3(grid),
+        launch_main((conv_dma_kernel<c.tc, c.tp, c.wc, c.wp, c.ns, false, c.sh, c.ks>), dim3(grid),
                            dim3(c.wc * c.wp * 64 * c.ks), 0, st, a);
     return hipGetLastError();
 }

@@ -391,9 +391,9 @@ static hipError_t launch_halo_nw(const ConvArgs &a, const HaloGeom &g, hipStream
     const size_t lds = halo_lds_bytes(a, NW);
     const dim3 grid((unsigned)(a.tiles_c * g.nwg_p));
     if (a.flip4)
-        hipLaunchKernelGGL((conv_halo_kernel<NW, true>), grid, dim3(NW * 64), lds, st, a, g);
+        launch_main((conv_halo_kernel<NW, true>), grid, dim3(NW * 64), lds, st, a, g);
     else
-        hipLaunchKernelGGL((conv_halo_kernel<NW, false>), grid, dim3(NW * 64), lds, st, a, g);
+        launch_main((conv_halo_kernel<NW, false>), grid, dim3(NW * 64), lds, st, a, g);
     return hipGetLastError();
 }
 

@@ -623,7 +623,7 @@ static hipError_t launch_cfg(const ConvArgs &a, hipStream_t st)
 {
     dim3 grid(a.nblocks), block(256);
     const unsigned dyn = a.chan_in_lds ? (unsigned)(a.Kpad * sizeof(ChanRec)) : 0u;
-    hipLaunchKernelGGL((conv_mfma_kernel<TC, TP, BK, WC, WP, AVEC, ring_depth<TC, TP>()>), grid, block, dyn, st, a);
+    launch_main((conv_mfma_kernel<TC, TP, BK, WC, WP, AVEC, ring_depth<TC, TP>()>), grid, block, dyn, st, a);
     return hipGetLastError();
 }
 

@@ -278,7 +278,7 @@ static hipError_t launch_tap_cfg(const ConvArgs &a, hipStream_t st)
 {
     constexpr TapCfg c = kTapCfg[T];
     const int grid = (a.ntiles + 7) / 8 * 8;
-    hipLaunchKernelGGL((conv_tap_kernel<c.tc, c.tp, c.bk, c.wc, c.wp>), dim3(grid), dim3(c.wc * c.wp * 64), 0, st,
+    launch_main((conv_tap_kernel<c.tc, c.tp, c.bk, c.wc, c.wp>), dim3(grid), dim3(c.wc * c.wp * 64), 0, st,
                        a);
     return hipGetLastError();
 }

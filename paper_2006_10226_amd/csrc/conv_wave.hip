@@ -424,9 +424,9 @@ static hipError_t launch_wave_split(const ConvArgs &a, hipStream_t st)
     const int grid = (nwg + 7) / 8 * 8;
     const dim3 block(wave_count<KSPLIT>() * 64);
     if (a.flip4)
-        hipLaunchKernelGGL((conv_wave_kernel<KSPLIT, 4, true>), dim3(grid), block, 0, st, a);
+        launch_main((conv_wave_kernel<KSPLIT, 4, true>), dim3(grid), block, 0, st, a);
     else
-        hipLaunchKernelGGL((conv_wave_kernel<KSPLIT, 4, false>), dim3(grid), block, 0, st, a);
+        launch_main((conv_wave_kernel<KSPLIT, 4, false>), dim3(grid), block, 0, st, a);
     return hipGetLastError();
 }
 

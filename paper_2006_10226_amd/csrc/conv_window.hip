@@ -476,9 +476,9 @@ static hipError_t launch_win_cfg(const ConvArgs &a, const WinGeom &g, hipStream_
     const dim3 grid((unsigned)(a.tiles_c * g.ngrp));
     const dim3 block(64 * c.nb * c.ks);
     if (a.flip4)
-        hipLaunchKernelGGL((conv_window_kernel<c.nb, c.ks, c.tcb, true>), grid, block, lds, st, a, g);
+        launch_main((conv_window_kernel<c.nb, c.ks, c.tcb, true>), grid, block, lds, st, a, g);
     else
-        hipLaunchKernelGGL((conv_window_kernel<c.nb, c.ks, c.tcb, false>), grid, block, lds, st, a, g);
+        launch_main((conv_window_kernel<c.nb, c.ks, c.tcb, false>), grid, block, lds, st, a, g);
     return hipGetLastError();
 }
 

@@ -226,7 +226,7 @@ hipError_t launch_prep_dw3(const int8_t *w, const int32_t *bias, int C, int32_t 
 template <int SW, bool ZPW, int OUT>
 static void launch_dw3_cfg(const DwArgs &a, dim3 grid, hipStream_t st)
 {
-    hipLaunchKernelGGL((depthwise3_kernel<SW, kDw3Pixels, ZPW, OUT>), grid, dim3(256), 0, st, a);
+    launch_main((depthwise3_kernel<SW, kDw3Pixels, ZPW, OUT>), grid, dim3(256), 0, st, a);
 }
 
 template <int SW, bool ZPW>

@@ -108,11 +108,11 @@ hipError_t launch_depthwise(const DwArgs &a, hipStream_t st)
     const long long total = (long long)a.N * a.Ho * a.Wo * (vec ? a.C / 4 : a.C);
     dim3 grid((unsigned)((total + 255) / 256)), block(256);
     if (vec) {
-        if (a.out_i32) hipLaunchKernelGGL((depthwise_kernel<true, true>), grid, block, 0, st, a);
-        else hipLaunchKernelGGL((depthwise_kernel<true, false>), grid, block, 0, st, a);
+        if (a.out_i32) launch_main((depthwise_kernel<true, true>), grid, block, 0, st, a);
+        else launch_main((depthwise_kernel<true, false>), grid, block, 0, st, a);
     } else {
-        if (a.out_i32) hipLaunchKernelGGL((depthwise_kernel<false, true>), grid, block, 0, st, a);
-        else hipLaunchKernelGGL((depthwise_kernel<false, false>), grid, block, 0, st, a);
+        if (a.out_i32) launch_main((depthwise_kernel<false, true>), grid, block, 0, st, a);
+        else launch_main((depthwise_kernel<false, false>), grid, block, 0, st, a);
     }
     return hipGetLastError();
 }

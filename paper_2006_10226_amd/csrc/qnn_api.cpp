@@ -18,6 +18,12 @@
 
 using namespace qnn;
 
+qnn::LaunchEvents &qnn::launch_events()
+{
+    static thread_local LaunchEvents ev;
+    return ev;
+}
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -1670,6 +1676,23 @@ qnn_status qnn_plan_run(const qnn_plan *plan, void *stream, const void *x, void 
     if (!plan)
         return fail(QNN_ERR_NULL, "plan_run: plan is NULL");
     return run_plan(plan, (hipStream_t)stream, x, y, workspace);
+}
+
+qnn_status qnn_plan_run_timed(const qnn_plan *plan, void *stream, const void *x, void *y, void *workspace,
+                              void *start_event, void *stop_event)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_run_timed: plan is NULL");
+    if (!start_event || !stop_event)
+        return fail(QNN_ERR_NULL, "plan_run_timed: an event is NULL");
+    if (plan->kind != PLAN_CONV && plan->kind != PLAN_DW)
+        return fail(QNN_ERR_UNSUPPORTED, "plan_run_timed: conv, dense and depthwise plans only");
+    LaunchEvents &ev = launch_events();
+    ev.start = (hipEvent_t)start_event;
+    ev.stop = (hipEvent_t)stop_event;
+    const qnn_status s = run_plan(plan, (hipStream_t)stream, x, y, workspace);
+    ev = LaunchEvents{};
+    return s;
 }
 
 qnn_status qnn_plan_run_noalloc(const qnn_plan *plan, void *stream, const void *x, void *y)

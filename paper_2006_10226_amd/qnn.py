@@ -39,7 +39,7 @@ EXPORTS = [
     "qnn_conv2d", "qnn_depthwise_conv2d", "qnn_dense", "qnn_requantize", "qnn_add",
     "qnn_pool2d",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
-    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
+    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_timed", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
     "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
 ]
 
@@ -114,6 +114,8 @@ def lib() -> ctypes.CDLL:
     L.qnn_requantize_plan_create.restype = st
     L.qnn_plan_run.argtypes = [P, P, P, P, P]
     L.qnn_plan_run.restype = st
+    L.qnn_plan_run_timed.argtypes = [P, P, P, P, P, P, P]
+    L.qnn_plan_run_timed.restype = st
     L.qnn_plan_run_noalloc.argtypes = [P, P, P, P]
     L.qnn_plan_run_noalloc.restype = st
     L.qnn_plan_workspace_size.argtypes = [P]
@@ -267,6 +269,16 @@ class Plan:
                 self.workspace_size:
             raise ValueError("workspace is smaller than the plan needs")
         _check(lib().qnn_plan_run(self._h, _stream(stream), _ptr(x), _ptr(out), _ptr(workspace)))
+        return out
+
+    def run_timed(self, x: torch.Tensor, out: torch.Tensor, workspace, start, stop, stream=None):
+        """qnn_plan_run_timed: start / stop (torch.cuda.Event with timing)
+        are recorded at the main kernel's own start and end."""
+        for e in (start, stop):
+            if not e.cuda_event:   # torch creates its events on first record
+                e.record()
+        _check(lib().qnn_plan_run_timed(self._h, _stream(stream), _ptr(x), _ptr(out), _ptr(workspace),
+                                        ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event)))
         return out
 
     def run_noalloc(self, x: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:

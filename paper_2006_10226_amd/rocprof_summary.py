@@ -9,10 +9,18 @@ Reads
 and writes a markdown summary plus ``traffic.json``, which bench.py reads to
 fill ``roofline.traffic`` as long as the kernel sources are unchanged.
 
+and, when given, two more counter passes of the same bench command:
+  * --mfma D: SQ_INSTS_VALU_MFMA_MOPS_I8 (int8 MFMA work in units of 512
+    ops), SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE (MFMA busy fraction
+    = busy cycles summed over the SIMDs / (traced kernel duration x 2.4 GHz
+    x 1024 SIMDs); under counter collection GRBM_GUI_ACTIVE is stretched);
+  * --l2 D: TCC_HIT_sum, TCC_MISS_sum (L2 hit rate), TCP_TCC_READ_REQ_sum
+    and TCP_TCC_READ_REQ_LATENCY_sum (average L1-to-L2 read latency, cycles).
+
 Usage:
   python -m paper_2006_10226_amd.rocprof_summary --stats D --fetch D --write D \
       --copy-fetch D --copy-write D --copy-mib 512 --layers F --out-md F \
-      --out-json F --command "..." [--command "..."]
+      --out-json F [--mfma D] [--l2 D] --command "..." [--command "..."]
 """
 import argparse
 import csv
@@ -24,7 +32,8 @@ import re
 
 _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
 _TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
-_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)(?:, ?(\d+))?>")
+_DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)"
+                  r"(?:, ?(\d+))?(?:, ?(true|false))?>")
 _WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
 _HALO = re.compile(r"conv_halo_kernel<(\d+), ?(true|false)>")
 _WIN = re.compile(r"conv_window_kernel<(\d+), ?(\d+), ?(\d+), ?(true|false)>")
@@ -61,7 +70,8 @@ def group_of(kernel_name):
         tc, tp, wc, wp, ns = (int(v) for v in m.groups()[:5])
         short = "s" if m.group(7) == "true" else ""
         ks = int(m.group(8)) if m.group(8) else 1
-        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * ks * 64} stages={ns}{short}"
+        split = " ksplit" if m.group(9) == "true" else ""
+        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * ks * 64} stages={ns}{short}{split}"
     m = _WAVE.search(kernel_name)
     if m:
         split = int(m.group(1))
@@ -100,17 +110,30 @@ def read_stats(d):
 
 
 def read_counter(d, counter):
-    """Per kernel group: list of per-dispatch counter values (KiB)."""
-    per = {}
+    """Per kernel group: list of per-dispatch counter values (summed over the
+    counter's instances)."""
+    return {g: [v[counter] for v in rows] for g, rows in read_counters(d, [counter]).items()}
+
+
+def read_counters(d, counters):
+    """Per kernel group: list of per-dispatch dicts {counter: value}, for the
+    dispatches that report every one of `counters`."""
     vals = {}
     for r in csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))):
-        if r["Counter_Name"] != counter:
+        if r["Counter_Name"] not in counters:
             continue
         key = (r["Dispatch_Id"], r["Kernel_Name"])
-        vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
-    for (_, name), v in vals.items():
-        per.setdefault(group_of(name), []).append(v)
+        row = vals.setdefault(key, {})
+        row[r["Counter_Name"]] = row.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    per = {}
+    for (_, name), row in vals.items():
+        if all(c in row for c in counters):
+            per.setdefault(group_of(name), []).append(row)
     return per
+
+
+SIMDS = 256 * 4   # MI355X: 256 CUs of 4 SIMDs
+CLOCK_HZ = 2.4e9  # MI355X peak engine clock
 
 
 def main():
@@ -126,6 +149,9 @@ def main():
     ap.add_argument("--out-json", required=True)
     ap.add_argument("--command", action="append", default=[])
     ap.add_argument("--bench-json", help="the JSON line bench.py printed in the unprofiled run")
+    ap.add_argument("--mfma", help="--pmc SQ_INSTS_VALU_MFMA_MOPS_I8 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE directory")
+    ap.add_argument("--l2", help="--pmc TCC_HIT_sum TCC_MISS_sum TCP_TCC_READ_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum "
+                                 "directory")
     args = ap.parse_args()
 
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -151,7 +177,46 @@ def main():
         groups[g] = {"bytes_per_launch": round(rd + wr), "read_bytes_per_launch": round(rd),
                      "write_bytes_per_launch": round(wr),
                      "algorithmic_bytes_per_launch": round(d["bytes"] / d["launches"]),
-                     "dispatches_counted": len(fetch[g])}
+                     "dispatches_counted": len(fetch[g]), "layers": sorted(d.get("layers", []))}
+    # kernel time of each group from the trace (the duration bench.py's
+    # roofline line must agree with)
+    trace = {}
+    for st in stats:
+        gname = group_of(st["name"])
+        t = trace.setdefault(gname, [0, 0.0])
+        t[0] += st["calls"]
+        t[1] += st["total_ns"]
+    for g, d in layers["groups"].items():
+        if g in groups and g in trace:
+            groups[g]["trace_avg_us"] = round(trace[g][1] / trace[g][0] / 1e3, 3)
+            groups[g]["algorithmic_ops_per_launch"] = round(2 * d["macs"] / d["launches"])
+    if args.mfma:
+        mf = read_counters(args.mfma, ["SQ_INSTS_VALU_MFMA_MOPS_I8", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"])
+        for g, rows in mf.items():
+            if g not in groups:
+                continue
+            n = len(rows)
+            groups[g]["mfma_i8_ops_per_launch"] = round(sum(r["SQ_INSTS_VALU_MFMA_MOPS_I8"] for r in rows) / n * 512)
+            busy = sum(r["SQ_VALU_MFMA_BUSY_CYCLES"] for r in rows) / n
+            groups[g]["mfma_busy_cycles_per_launch"] = round(busy)
+            # busy cycles summed over the SIMDs, over the kernel's traced
+            # duration at the 2.4 GHz peak clock times 1024 SIMDs (the
+            # counter passes themselves stretch GRBM_GUI_ACTIVE)
+            t = groups[g].get("trace_avg_us")
+            if t:
+                groups[g]["mfma_busy"] = round(busy / (t * 1e-6 * CLOCK_HZ * SIMDS), 4)
+    if args.l2:
+        l2 = read_counters(args.l2, ["TCC_HIT_sum", "TCC_MISS_sum", "TCP_TCC_READ_REQ_sum",
+                                     "TCP_TCC_READ_REQ_LATENCY_sum"])
+        for g, rows in l2.items():
+            if g not in groups:
+                continue
+            hit = sum(r["TCC_HIT_sum"] for r in rows)
+            miss = sum(r["TCC_MISS_sum"] for r in rows)
+            req = sum(r["TCP_TCC_READ_REQ_sum"] for r in rows)
+            lat = sum(r["TCP_TCC_READ_REQ_LATENCY_sum"] for r in rows)
+            groups[g]["l2_hit_rate"] = round(hit / max(1.0, hit + miss), 4)
+            groups[g]["l1_to_l2_read_latency_cycles"] = round(lat / max(1.0, req), 1)
     rec = {"source_sha1": sha, "copy_mib": args.copy_mib, "fetch_scale": f_read, "write_scale": f_write,
            "workload": layers["workload"], "groups": groups}
     with open(args.out_json, "w") as f:
@@ -205,6 +270,35 @@ def main():
         lines.append(f"| {g} | {d['read_bytes_per_launch'] / 1e6:.3f} | {d['write_bytes_per_launch'] / 1e6:.3f} |"
                      f" {d['bytes_per_launch'] / 1e6:.3f} | {d['algorithmic_bytes_per_launch'] / 1e6:.3f} |"
                      f" {d['bytes_per_launch'] / max(1, d['algorithmic_bytes_per_launch']):.2f} |")
+    lines.append("")
+    if args.mfma or args.l2:
+        lines.append("## Matrix cores and L2 (--pmc SQ_INSTS_VALU_MFMA_MOPS_I8 SQ_VALU_MFMA_BUSY_CYCLES "
+                     "GRBM_GUI_ACTIVE; --pmc TCC_HIT_sum TCC_MISS_sum TCP_TCC_READ_REQ_sum "
+                     "TCP_TCC_READ_REQ_LATENCY_sum)")
+        lines.append("")
+        lines.append("MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the SIMDs; 16 per 16x16x64 int8 MFMA) / "
+                     "(traced kernel duration x 2.4 GHz x 1024 SIMDs); int8 MFMA ops = "
+                     "SQ_INSTS_VALU_MFMA_MOPS_I8 x 512, beside the algorithmic 2 x MACs (the difference is the "
+                     "padding of the reduction and of partial tiles); L2 hit rate = TCC_HIT / (TCC_HIT + TCC_MISS); "
+                     "L1-to-L2 read latency = TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ (cycles).")
+        lines.append("")
+        lines.append("| kernel group | layers | trace avg us | algorithmic GOP/launch | MFMA int8 GOP/launch |"
+                     " MFMA busy | TOP/s (trace) | L2 hit rate | L1->L2 read latency (cycles) |")
+        lines.append("|---|---|---|---|---|---|---|---|---|")
+        for g, d in groups.items():
+            ops = d.get("algorithmic_ops_per_launch", 0)
+            t = d.get("trace_avg_us")
+            tops = f"{ops / (t * 1e-6) / 1e12:.1f}" if t and ops else "-"
+            mops = d.get("mfma_i8_ops_per_launch")
+            lines.append(f"| {g} | {len(d['layers'])} | {t if t else '-'} | {ops / 1e9:.3f} |"
+                         f" {mops / 1e9 if mops is not None else float('nan'):.3f} |"
+                         f" {d.get('mfma_busy', float('nan')):.3f} | {tops} | {d.get('l2_hit_rate', float('nan')):.3f} |"
+                         f" {d.get('l1_to_l2_read_latency_cycles', float('nan'))} |")
+        lines.append("")
+    lines.append("## Layers of each group")
+    lines.append("")
+    for g, d in groups.items():
+        lines.append(f"- {g}: {', '.join(d['layers'])}")
     lines.append("")
     with open(args.out_md, "w") as f:
         f.write("\n".join(lines))
