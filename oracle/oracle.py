@@ -56,11 +56,11 @@ def _load():
     lib.oracle_pool2d.restype = ctypes.c_int
     lib.oracle_conv_out_hw.argtypes = [P, P, P, P]
     lib.oracle_conv_out_hw.restype = None
-    lib.oracle_conv2d_acc.argtypes = [P, i32, i32, P, P, P, P, P, i32, P]
+    lib.oracle_conv2d_acc.argtypes = [P, i32, i32, P, i32, P, P, P, P, i32, P]
     lib.oracle_conv2d_acc.restype = None
-    lib.oracle_conv2d_acc_points.argtypes = [P, i32, i32, P, P, P, P, P, i32, P, i64, P]
+    lib.oracle_conv2d_acc_points.argtypes = [P, i32, i32, P, i32, P, P, P, P, i32, P, i64, P]
     lib.oracle_conv2d_acc_points.restype = None
-    lib.oracle_dense_acc.argtypes = [P, i32, i32, P, P, P, i64, i64, i64, P]
+    lib.oracle_dense_acc.argtypes = [P, i32, i32, P, i32, P, P, i64, i64, i64, P]
     lib.oracle_dense_acc.restype = None
     lib.oracle_requantize_acc.argtypes = [P, i64, i64, f32, P, i32, f32, i32, i32,
                                           i64, i64, i32, P, i64, i64]
@@ -146,11 +146,17 @@ def conv_out_hw(H, W, R, S, stride=(1, 1), pads=(0, 0, 0, 0), dil=(1, 1)):
     return ho.value, wo.value
 
 
+def _weights(w):
+    """Weights as given when uint8 (asymmetric uint8 weights), else int8."""
+    w = np.ascontiguousarray(w)
+    return w if w.dtype == np.uint8 else _c(w, np.int8)
+
+
 def _conv_args(x, w, zp_w, bias, stride, pads, dil, depthwise):
     x = np.ascontiguousarray(x)
     if x.dtype not in DTYPE_CODE or x.dtype == np.int32:
         raise TypeError("activations must be uint8 or int8")
-    w = _c(w, np.int8)
+    w = _weights(w)
     N, H, W, C = x.shape
     if depthwise:
         R, S, Cw = w.shape
@@ -178,7 +184,7 @@ def conv2d_acc(x, zp_x, w, zp_w=0, bias=None, stride=(1, 1), pads=(0, 0, 0, 0),
     N, H, W, C, K, R, S = dims
     Ho, Wo = conv_out_hw(H, W, R, S, stride, pads, dil)
     acc = np.empty((N, Ho, Wo, K), np.int64)
-    _load().oracle_conv2d_acc(_ptr(x), DTYPE_CODE[x.dtype], int(zp_x), _ptr(w), _ptr(zpw),
+    _load().oracle_conv2d_acc(_ptr(x), DTYPE_CODE[x.dtype], int(zp_x), _ptr(w), DTYPE_CODE[w.dtype], _ptr(zpw),
                               _ptr(b), _ptr(shape), _ptr(cp), int(bool(depthwise)), _ptr(acc))
     return acc
 
@@ -189,7 +195,8 @@ def conv2d_acc_points(x, zp_x, w, idx, zp_w=0, bias=None, stride=(1, 1),
     x, w, zpw, b, shape, cp, _ = _conv_args(x, w, zp_w, bias, stride, pads, dil, depthwise)
     idx = _c(idx, np.int64)
     acc = np.empty(idx.shape, np.int64)
-    _load().oracle_conv2d_acc_points(_ptr(x), DTYPE_CODE[x.dtype], int(zp_x), _ptr(w), _ptr(zpw),
+    _load().oracle_conv2d_acc_points(_ptr(x), DTYPE_CODE[x.dtype], int(zp_x), _ptr(w), DTYPE_CODE[w.dtype],
+                                     _ptr(zpw),
                                      _ptr(b), _ptr(shape), _ptr(cp), int(bool(depthwise)),
                                      _ptr(idx), idx.size, _ptr(acc))
     return acc
@@ -198,7 +205,7 @@ def conv2d_acc_points(x, zp_x, w, idx, zp_w=0, bias=None, stride=(1, 1),
 def dense_acc(x, zp_x, w, zp_w=0, bias=None):
     """int64 acc[m, n] = bias[n] + sum_k (x[m,k]-zp_x) * (w[n,k]-zp_w[n])."""
     x = np.ascontiguousarray(x)
-    w = _c(w, np.int8)
+    w = _weights(w)
     M, Kd = x.shape
     Nd, Kw = w.shape
     if Kw != Kd:
@@ -206,7 +213,8 @@ def dense_acc(x, zp_x, w, zp_w=0, bias=None):
     zpw = _per_channel(zp_w, Nd, np.int32)
     b = None if bias is None else _c(bias, np.int32)
     acc = np.empty((M, Nd), np.int64)
-    _load().oracle_dense_acc(_ptr(x), DTYPE_CODE[x.dtype], int(zp_x), _ptr(w), _ptr(zpw), _ptr(b),
+    _load().oracle_dense_acc(_ptr(x), DTYPE_CODE[x.dtype], int(zp_x), _ptr(w), DTYPE_CODE[w.dtype], _ptr(zpw),
+                             _ptr(b),
                              M, Kd, Nd, _ptr(acc))
     return acc
 

@@ -252,9 +252,11 @@ static int64_t x_padded(const void *x, int xt, const conv_geom *g, int64_t n,
  * One conv2d accumulator (Eq. (2)/(3) in product form) plus bias:
  *   acc = bias[k] + sum_{r,s,c} (x~[n, oh*sh + r*dh - pt, ow*sw + s*dw - pl, c]
  *                                 - zp_x) * (w[k,r,s,c] - zp_w[k])
- * with w in OHWI order.
+ * with w in OHWI order, of dtype wt: int8, or uint8 as in pre-quantized
+ * models whose weights are asymmetric uint8 (the weight zero point is then
+ * in [0, 255]).
  */
-static int64_t conv_acc_one(const void *x, int xt, int64_t zp_x, const int8_t *w,
+static int64_t conv_acc_one(const void *x, int xt, int64_t zp_x, const void *w, int wt,
                             const int32_t *zp_w, const int32_t *bias,
                             const conv_geom *g, int64_t n, int64_t oh,
                             int64_t ow, int64_t k)
@@ -266,7 +268,7 @@ static int64_t conv_acc_one(const void *x, int xt, int64_t zp_x, const int8_t *w
                 int64_t ih = oh * g->sh + r * g->dh - g->pt;
                 int64_t iw = ow * g->sw + s * g->dw - g->pl;
                 int64_t a = x_padded(x, xt, g, n, ih, iw, c, zp_x) - zp_x;
-                int64_t b = (int64_t)w[((k * g->R + r) * g->S + s) * g->C + c] - zp_w[k];
+                int64_t b = q_load(w, wt, ((k * g->R + r) * g->S + s) * g->C + c) - zp_w[k];
                 acc += a * b;
             }
     if (bias)
@@ -275,7 +277,7 @@ static int64_t conv_acc_one(const void *x, int xt, int64_t zp_x, const int8_t *w
 }
 
 /* Depthwise (channel multiplier 1): w is [R][S][C]. */
-static int64_t dw_acc_one(const void *x, int xt, int64_t zp_x, const int8_t *w,
+static int64_t dw_acc_one(const void *x, int xt, int64_t zp_x, const void *w, int wt,
                           const int32_t *zp_w, const int32_t *bias,
                           const conv_geom *g, int64_t n, int64_t oh,
                           int64_t ow, int64_t c)
@@ -286,7 +288,7 @@ static int64_t dw_acc_one(const void *x, int xt, int64_t zp_x, const int8_t *w,
             int64_t ih = oh * g->sh + r * g->dh - g->pt;
             int64_t iw = ow * g->sw + s * g->dw - g->pl;
             int64_t a = x_padded(x, xt, g, n, ih, iw, c, zp_x) - zp_x;
-            int64_t b = (int64_t)w[(r * g->S + s) * g->C + c] - zp_w[c];
+            int64_t b = q_load(w, wt, (r * g->S + s) * g->C + c) - zp_w[c];
             acc += a * b;
         }
     if (bias)
@@ -307,7 +309,7 @@ void oracle_conv_out_hw(const int32_t *shape, const int32_t *cp, int64_t *ho, in
  * depthwise != 0 selects the channel-multiplier-1 depthwise form, where
  * shape[4] (K) must equal C and w is [R][S][C].
  */
-void oracle_conv2d_acc(const void *x, int32_t xt, int32_t zp_x, const int8_t *w,
+void oracle_conv2d_acc(const void *x, int32_t xt, int32_t zp_x, const void *w, int32_t wt,
                        const int32_t *zp_w, const int32_t *bias,
                        const int32_t *shape, const int32_t *cp, int32_t depthwise,
                        int64_t *acc)
@@ -321,14 +323,14 @@ void oracle_conv2d_acc(const void *x, int32_t xt, int32_t zp_x, const int8_t *w,
             for (int64_t k = 0; k < g.K; ++k) {
                 int64_t m = (n * g.Ho + oh) * g.Wo + ow;
                 acc[m * g.K + k] = depthwise
-                    ? dw_acc_one(x, xt, zp_x, w, zp_w, bias, &g, n, oh, ow, k)
-                    : conv_acc_one(x, xt, zp_x, w, zp_w, bias, &g, n, oh, ow, k);
+                    ? dw_acc_one(x, xt, zp_x, w, wt, zp_w, bias, &g, n, oh, ow, k)
+                    : conv_acc_one(x, xt, zp_x, w, wt, zp_w, bias, &g, n, oh, ow, k);
             }
     }
 }
 
 /* Accumulators at selected flat output indices idx = m * K + k only. */
-void oracle_conv2d_acc_points(const void *x, int32_t xt, int32_t zp_x, const int8_t *w,
+void oracle_conv2d_acc_points(const void *x, int32_t xt, int32_t zp_x, const void *w, int32_t wt,
                               const int32_t *zp_w, const int32_t *bias,
                               const int32_t *shape, const int32_t *cp, int32_t depthwise,
                               const int64_t *idx, int64_t npts, int64_t *acc)
@@ -339,13 +341,13 @@ void oracle_conv2d_acc_points(const void *x, int32_t xt, int32_t zp_x, const int
         int64_t m = idx[i] / g.K, k = idx[i] % g.K;
         int64_t ow = m % g.Wo, oh = (m / g.Wo) % g.Ho, n = m / (g.Wo * g.Ho);
         acc[i] = depthwise
-            ? dw_acc_one(x, xt, zp_x, w, zp_w, bias, &g, n, oh, ow, k)
-            : conv_acc_one(x, xt, zp_x, w, zp_w, bias, &g, n, oh, ow, k);
+            ? dw_acc_one(x, xt, zp_x, w, wt, zp_w, bias, &g, n, oh, ow, k)
+            : conv_acc_one(x, xt, zp_x, w, wt, zp_w, bias, &g, n, oh, ow, k);
     }
 }
 
 /* Dense: acc[m][j] = bias[j] + sum_k (x[m,k] - zp_x) * (w[j,k] - zp_w[j]). */
-void oracle_dense_acc(const void *x, int32_t xt, int32_t zp_x, const int8_t *w,
+void oracle_dense_acc(const void *x, int32_t xt, int32_t zp_x, const void *w, int32_t wt,
                       const int32_t *zp_w, const int32_t *bias, int64_t M,
                       int64_t Kd, int64_t Nd, int64_t *acc)
 {
@@ -355,7 +357,7 @@ void oracle_dense_acc(const void *x, int32_t xt, int32_t zp_x, const int8_t *w,
             int64_t a = 0;
             for (int64_t k = 0; k < Kd; ++k)
                 a += (q_load(x, xt, m * Kd + k) - zp_x) *
-                     ((int64_t)w[j * Kd + k] - zp_w[j]);
+                     (q_load(w, wt, j * Kd + k) - zp_w[j]);
             if (bias)
                 a += bias[j];
             acc[m * Nd + j] = a;

@@ -221,3 +221,56 @@ def test_points_match_full(oracle):
     idx = W.sample_indices(acc.size, 3000, seed=4)
     pts = oracle.conv2d_acc_points(c.x, c.zp_x, c.w, idx, c.zp_w, c.bias, c.stride, c.pads)
     np.testing.assert_array_equal(pts, acc.reshape(-1)[idx])
+
+
+@pytest.mark.parametrize("depthwise", [False, True])
+def test_uint8_weights_match_float64_library(oracle, depthwise):
+    """Asymmetric uint8 weights (zero points in [0, 255]): the oracle's
+    accumulator equals float64 library convolution of (Q_x - zp_x) and
+    (Q_w - zp_w) with zero padding (exact: every partial sum is an integer
+    below 2^53), for stride, asymmetric padding and per-channel zero points."""
+    rng = np.random.default_rng(41)
+    C = 6
+    K = C if depthwise else 5
+    x = rng.integers(0, 256, size=(2, 9, 8, C), dtype=np.uint8)
+    w = (rng.integers(0, 256, size=(3, 2, C), dtype=np.uint8) if depthwise
+         else rng.integers(0, 256, size=(K, 3, 2, C), dtype=np.uint8))
+    zp_w = rng.integers(0, 256, size=K).astype(np.int32)
+    bias = rng.integers(-999, 1000, size=K).astype(np.int32)
+    stride, pads = (2, 1), (1, 0, 2, 1)
+    acc = oracle.conv2d_acc(x, 131, w, zp_w, bias, stride, pads, depthwise=depthwise)
+    xt = torch.from_numpy(x.astype(np.float64) - 131).permute(0, 3, 1, 2)
+    xt = F.pad(xt, (pads[1], pads[3], pads[0], pads[2]))
+    if depthwise:
+        wt = torch.from_numpy(w.astype(np.float64) - zp_w[None, None, :]).permute(2, 0, 1)[:, None]
+        ref = F.conv2d(xt, wt, stride=stride, groups=C)
+    else:
+        wt = torch.from_numpy(w.astype(np.float64) - zp_w[:, None, None, None]).permute(0, 3, 1, 2)
+        ref = F.conv2d(xt, wt, stride=stride)
+    ref = ref.permute(0, 2, 3, 1).numpy() + bias
+    np.testing.assert_array_equal(acc, ref.astype(np.int64))
+
+
+def test_uint8_weights_dequantize_identity(oracle):
+    """Eq. (1)/(2) with uint8 weights: the real conv of s_x(Q_x - zp_x) and
+    s_w(Q_w - zp_w) (real 0.0 in the padding) equals s_x*s_w[k]*acc, exactly."""
+    rng = np.random.default_rng(42)
+    x = rng.integers(0, 256, size=(1, 4, 5, 2), dtype=np.uint8)
+    w = rng.integers(0, 256, size=(3, 2, 2, 2), dtype=np.uint8)
+    zp_w = [200, 3, 128]
+    s_w = [float(np.float32(v)) for v in (0.01, 0.003, 0.02)]
+    acc = oracle.conv2d_acc(x, 77, w, np.array(zp_w, np.int32), None, (1, 2), (1, 1, 0, 1))
+    real = X.conv2d_real(x.tolist(), 0.05, 77, w.tolist(), s_w, zp_w, None, (1, 2), (1, 1, 0, 1))
+    for idx in np.ndindex(acc.shape):
+        assert real[idx[0]][idx[1]][idx[2]][idx[3]] == X.f32(0.05) * X.f32(s_w[idx[3]]) * int(acc[idx])
+
+
+def test_uint8_weights_dense_brute_force(oracle):
+    rng = np.random.default_rng(43)
+    x = rng.integers(-128, 128, size=(3, 7), dtype=np.int8)
+    w = rng.integers(0, 256, size=(4, 7), dtype=np.uint8)
+    zp_w = np.array([0, 255, 128, 17], np.int32)
+    acc = oracle.dense_acc(x, -5, w, zp_w, None)
+    for m in range(3):
+        for j in range(4):
+            assert acc[m, j] == sum((int(x[m, k]) + 5) * (int(w[j, k]) - int(zp_w[j])) for k in range(7))
