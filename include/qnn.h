@@ -290,6 +290,43 @@ qnn_status qnn_dense_plan_create(qnn_plan **plan, void *stream,
                                  const int32_t *bias, qnn_dtype y_dtype, qnn_qparams y_q,
                                  qnn_clamp act, qnn_rounding rounding, int32_t y_ldc);
 
+/*
+ * The same three plans for weights given as int8 or asymmetric uint8
+ * (w_dtype QNN_INT8 or QNN_UINT8; with uint8 the weight zero points lie in
+ * [0, 255]).  Pre-quantized models of some frameworks carry uint8 weights;
+ * as Sec. III-C legalises a dtype the instructions do not take (there the
+ * activations of Intel's uint8 x int8 dot products), uint8 weights are
+ * legalised once at creation: w' = w - 128 read as int8, zp_w' = zp_w - 128,
+ * which leaves every (w - zp_w) of Eq. (3), hence every output, unchanged.
+ * Everything else as in the plain creation calls; other dtypes return
+ * QNN_ERR_DTYPE.
+ */
+qnn_status qnn_conv2d_plan_create_wt(qnn_plan **plan, void *stream,
+                                     qnn_dtype x_dtype, int32_t N, int32_t H, int32_t W,
+                                     int32_t C, qnn_qparams x_q,
+                                     const void *w, qnn_dtype w_dtype, int32_t K, int32_t R,
+                                     int32_t S, qnn_qparams w_q, const int32_t *bias,
+                                     qnn_conv_params conv, qnn_dtype y_dtype, qnn_qparams y_q,
+                                     qnn_clamp act, qnn_rounding rounding, int32_t y_ldc,
+                                     int32_t y_coff);
+
+qnn_status qnn_depthwise_conv2d_plan_create_wt(qnn_plan **plan, void *stream,
+                                               qnn_dtype x_dtype, int32_t N, int32_t H,
+                                               int32_t W, int32_t C, qnn_qparams x_q,
+                                               const void *w, qnn_dtype w_dtype, int32_t R,
+                                               int32_t S, qnn_qparams w_q, const int32_t *bias,
+                                               qnn_conv_params conv, qnn_dtype y_dtype,
+                                               qnn_qparams y_q, qnn_clamp act,
+                                               qnn_rounding rounding, int32_t y_ldc,
+                                               int32_t y_coff);
+
+qnn_status qnn_dense_plan_create_wt(qnn_plan **plan, void *stream,
+                                    qnn_dtype x_dtype, int32_t M, int32_t Kd, qnn_qparams x_q,
+                                    const void *w, qnn_dtype w_dtype, int32_t Nd,
+                                    qnn_qparams w_q, const int32_t *bias, qnn_dtype y_dtype,
+                                    qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding,
+                                    int32_t y_ldc);
+
 /* Per-channel standalone requantize prepared once (count fixed). */
 qnn_status qnn_requantize_plan_create(qnn_plan **plan, void *stream,
                                       qnn_dtype x_dtype, int64_t count, int32_t channels,

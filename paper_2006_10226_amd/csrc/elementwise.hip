@@ -11,6 +11,8 @@
 // requantizes each operand to the output scale and sums them.
 #include "qnn_internal.h"
 
+#include <algorithm>
+
 namespace qnn {
 
 __device__ __forceinline__ int clampll(long long v, int lo, int hi)
@@ -333,6 +335,23 @@ __global__ void __launch_bounds__(256) cache_sweep_kernel(const uint4 *buf, long
     }
     if (acc == 0xffffffffu)
         *sink = (int)acc;
+}
+
+// Legalisation of uint8 weights at plan creation (Sec. III-C): w' = w - 128
+// as int8, i.e. each byte XOR 0x80 (the zero point shifts by the same 128).
+__global__ void __launch_bounds__(256) flip_bytes_kernel(const uint8_t *in, uint8_t *out, size_t n)
+{
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        out[i] = in[i] ^ 0x80u;
+}
+
+hipError_t launch_flip_bytes(const uint8_t *in, uint8_t *out, size_t n, hipStream_t st)
+{
+    if (n == 0)
+        return hipSuccess;
+    const size_t blocks = std::min<size_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(flip_bytes_kernel, dim3((unsigned)blocks), dim3(256), 0, st, in, out, n);
+    return hipGetLastError();
 }
 
 hipError_t launch_cache_sweep(const void *buf, size_t bytes, int *sink, hipStream_t st)

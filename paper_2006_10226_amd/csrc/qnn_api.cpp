@@ -1332,6 +1332,53 @@ qnn_status make_req_plan(qnn_dtype xt, int64_t count, int32_t channels, qnn_qpar
     return QNN_OK;
 }
 
+// ---------------------------------------------------------------- uint8 weights
+//
+// Weights given as asymmetric uint8 are legalised once, when the plan is
+// created, the way Sec. III-C legalises activations: w' = w - 128 (each
+// byte XOR 0x80, read as int8) and zp_w' = zp_w - 128, which leaves every
+// (w - zp_w), hence the accumulator, unchanged.  The int8 copy lives in a
+// temporary device buffer for the plan's preparation kernels only.
+struct LegalWeights {
+    void *dev = nullptr;
+    std::vector<int32_t> zp;
+    qnn_qparams q{};
+    ~LegalWeights()
+    {
+        if (dev)
+            (void)hipFree(dev);
+    }
+};
+
+qnn_status legalize_weights(const void *w, qnn_dtype wt, size_t n, const qnn_qparams &wq, int32_t channels,
+                            hipStream_t st, LegalWeights *out, const int8_t **w8, qnn_qparams *wq8)
+{
+    if (wt == QNN_INT8) {
+        *w8 = (const int8_t *)w;
+        *wq8 = wq;
+        return QNN_OK;
+    }
+    if (wt != QNN_UINT8)
+        return fail(QNN_ERR_DTYPE, "weights must be int8 or uint8");
+    qnn_status s = check_qparams(wq, "w qparams", channels, QNN_UINT8, true);
+    if (s != QNN_OK)
+        return s;
+    if (!w)
+        return fail(QNN_ERR_NULL, "weight pointer is NULL");
+    out->zp.assign(wq.zero_point, wq.zero_point + wq.n);
+    for (int32_t &z : out->zp)
+        z -= 128;
+    out->q = qnn_qparams{wq.scale, out->zp.data(), wq.n};
+    hipError_t e;
+    if (n && (e = hipMalloc(&out->dev, n)) != hipSuccess)
+        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes for the legalised weights failed", n);
+    if (n && (e = launch_flip_bytes((const uint8_t *)w, (uint8_t *)out->dev, n, st)) != hipSuccess)
+        return hip_fail(e, "weight legalisation launch");
+    *w8 = (const int8_t *)out->dev;
+    *wq8 = out->q;
+    return QNN_OK;
+}
+
 // ---------------------------------------------------------------- allocation-free runs
 //
 // qnn_plan_run_noalloc takes its workspace from this file-scope device
@@ -1658,6 +1705,66 @@ qnn_status qnn_dense_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtyp
     }
     *plan = p;
     return s;
+}
+
+qnn_status qnn_conv2d_plan_create_wt(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t N, int32_t H,
+                                     int32_t W, int32_t C, qnn_qparams x_q, const void *w, qnn_dtype w_dtype,
+                                     int32_t K, int32_t R, int32_t S, qnn_qparams w_q, const int32_t *bias,
+                                     qnn_conv_params conv, qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act,
+                                     qnn_rounding rounding, int32_t y_ldc, int32_t y_coff)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    const size_t n = K > 0 && R > 0 && S > 0 && C > 0 ? (size_t)K * R * S * C : 0;
+    LegalWeights lw;
+    const int8_t *w8 = nullptr;
+    qnn_qparams wq8{};
+    qnn_status s = legalize_weights(w, w_dtype, n, w_q, K, (hipStream_t)stream, &lw, &w8, &wq8);
+    if (s != QNN_OK)
+        return s;
+    return qnn_conv2d_plan_create(plan, stream, x_dtype, N, H, W, C, x_q, w8, K, R, S, wq8, bias, conv, y_dtype,
+                                  y_q, act, rounding, y_ldc, y_coff);
+}
+
+qnn_status qnn_depthwise_conv2d_plan_create_wt(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t N,
+                                               int32_t H, int32_t W, int32_t C, qnn_qparams x_q, const void *w,
+                                               qnn_dtype w_dtype, int32_t R, int32_t S, qnn_qparams w_q,
+                                               const int32_t *bias, qnn_conv_params conv, qnn_dtype y_dtype,
+                                               qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding, int32_t y_ldc,
+                                               int32_t y_coff)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    const size_t n = R > 0 && S > 0 && C > 0 ? (size_t)R * S * C : 0;
+    LegalWeights lw;
+    const int8_t *w8 = nullptr;
+    qnn_qparams wq8{};
+    qnn_status s = legalize_weights(w, w_dtype, n, w_q, C, (hipStream_t)stream, &lw, &w8, &wq8);
+    if (s != QNN_OK)
+        return s;
+    return qnn_depthwise_conv2d_plan_create(plan, stream, x_dtype, N, H, W, C, x_q, w8, R, S, wq8, bias, conv,
+                                            y_dtype, y_q, act, rounding, y_ldc, y_coff);
+}
+
+qnn_status qnn_dense_plan_create_wt(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t M, int32_t Kd,
+                                    qnn_qparams x_q, const void *w, qnn_dtype w_dtype, int32_t Nd, qnn_qparams w_q,
+                                    const int32_t *bias, qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act,
+                                    qnn_rounding rounding, int32_t y_ldc)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_create: plan pointer is NULL");
+    *plan = nullptr;
+    const size_t n = Nd > 0 && Kd > 0 ? (size_t)Nd * Kd : 0;
+    LegalWeights lw;
+    const int8_t *w8 = nullptr;
+    qnn_qparams wq8{};
+    qnn_status s = legalize_weights(w, w_dtype, n, w_q, Nd, (hipStream_t)stream, &lw, &w8, &wq8);
+    if (s != QNN_OK)
+        return s;
+    return qnn_dense_plan_create(plan, stream, x_dtype, M, Kd, x_q, w8, Nd, wq8, bias, y_dtype, y_q, act, rounding,
+                                 y_ldc);
 }
 
 qnn_status qnn_requantize_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int64_t count,

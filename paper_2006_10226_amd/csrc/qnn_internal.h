@@ -332,6 +332,7 @@ hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, h
 // Reads `bytes` (a multiple of 16) of `buf` through the caches (kernel
 // tuning uses it to evict what a timed launch would otherwise find cached).
 hipError_t launch_cache_sweep(const void *buf, size_t bytes, int *sink, hipStream_t st);
+hipError_t launch_flip_bytes(const uint8_t *in, uint8_t *out, size_t n, hipStream_t st);
 hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned, hipStream_t st);
 
 // Quantized pool2d (Eq. (4)): NHWC input and output of one dtype; mode 0

@@ -39,6 +39,7 @@ EXPORTS = [
     "qnn_conv2d", "qnn_depthwise_conv2d", "qnn_dense", "qnn_requantize", "qnn_add",
     "qnn_pool2d",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
+    "qnn_conv2d_plan_create_wt", "qnn_depthwise_conv2d_plan_create_wt", "qnn_dense_plan_create_wt",
     "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_timed", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
     "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
 ]
@@ -110,6 +111,15 @@ def lib() -> ctypes.CDLL:
     L.qnn_dense_plan_create.argtypes = [PP, P, st, i32, i32, QParams, P, i32, QParams, P, st, QParams,
                                         Clamp, st, i32]
     L.qnn_dense_plan_create.restype = st
+    L.qnn_conv2d_plan_create_wt.argtypes = [PP, P, st, i32, i32, i32, i32, QParams, P, st, i32, i32, i32,
+                                            QParams, P, ConvParams, st, QParams, Clamp, st, i32, i32]
+    L.qnn_conv2d_plan_create_wt.restype = st
+    L.qnn_depthwise_conv2d_plan_create_wt.argtypes = [PP, P, st, i32, i32, i32, i32, QParams, P, st, i32, i32,
+                                                      QParams, P, ConvParams, st, QParams, Clamp, st, i32, i32]
+    L.qnn_depthwise_conv2d_plan_create_wt.restype = st
+    L.qnn_dense_plan_create_wt.argtypes = [PP, P, st, i32, i32, QParams, P, st, i32, QParams, P, st, QParams,
+                                           Clamp, st, i32]
+    L.qnn_dense_plan_create_wt.restype = st
     L.qnn_requantize_plan_create.argtypes = [PP, P, st, i64, i32, QParams, st, QParams, Clamp, st]
     L.qnn_requantize_plan_create.restype = st
     L.qnn_plan_run.argtypes = [P, P, P, P, P]
@@ -319,9 +329,15 @@ def conv2d_plan(x_shape, x_dtype, x_scale, x_zp, w: torch.Tensor, w_scale, w_zp,
     y_ldc = K if y_ldc is None else y_ldc
     xq, wq, yq = _Q(x_scale, x_zp, 1), _per_tensor_or_channel(w_scale, w_zp), _Q(y_scale, y_zp, 1)
     h = ctypes.c_void_p()
-    _check(lib().qnn_conv2d_plan_create(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], N, H, W, C, xq.q,
-                                        _ptr(w), K, R, S, wq.q, _ptr(bias), cp, _NAME_DT[y_dtype], yq.q,
-                                        _clamp(act), _ROUND[rounding], y_ldc, y_coff))
+    if w.dtype == torch.uint8:   # asymmetric uint8 weights, legalised at creation
+        _check(lib().qnn_conv2d_plan_create_wt(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], N, H, W, C,
+                                               xq.q, _ptr(w), UINT8, K, R, S, wq.q, _ptr(bias), cp,
+                                               _NAME_DT[y_dtype], yq.q, _clamp(act), _ROUND[rounding], y_ldc,
+                                               y_coff))
+    else:
+        _check(lib().qnn_conv2d_plan_create(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], N, H, W, C, xq.q,
+                                            _ptr(w), K, R, S, wq.q, _ptr(bias), cp, _NAME_DT[y_dtype], yq.q,
+                                            _clamp(act), _ROUND[rounding], y_ldc, y_coff))
     return Plan(h, x_shape, _DT_TORCH[_NAME_DT[x_dtype]], (N, Ho, Wo, K), _DT_TORCH[_NAME_DT[y_dtype]],
                 (N, Ho, Wo, y_ldc))
 
@@ -339,10 +355,16 @@ def depthwise_conv2d_plan(x_shape, x_dtype, x_scale, x_zp, w: torch.Tensor, w_sc
     y_ldc = C if y_ldc is None else y_ldc
     xq, wq, yq = _Q(x_scale, x_zp, 1), _per_tensor_or_channel(w_scale, w_zp), _Q(y_scale, y_zp, 1)
     h = ctypes.c_void_p()
-    _check(lib().qnn_depthwise_conv2d_plan_create(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], N, H, W,
-                                                  C, xq.q, _ptr(w), R, S, wq.q, _ptr(bias), cp,
-                                                  _NAME_DT[y_dtype], yq.q, _clamp(act), _ROUND[rounding],
-                                                  y_ldc, y_coff))
+    if w.dtype == torch.uint8:
+        _check(lib().qnn_depthwise_conv2d_plan_create_wt(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], N, H,
+                                                         W, C, xq.q, _ptr(w), UINT8, R, S, wq.q, _ptr(bias), cp,
+                                                         _NAME_DT[y_dtype], yq.q, _clamp(act), _ROUND[rounding],
+                                                         y_ldc, y_coff))
+    else:
+        _check(lib().qnn_depthwise_conv2d_plan_create(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], N, H, W,
+                                                      C, xq.q, _ptr(w), R, S, wq.q, _ptr(bias), cp,
+                                                      _NAME_DT[y_dtype], yq.q, _clamp(act), _ROUND[rounding],
+                                                      y_ldc, y_coff))
     return Plan(h, x_shape, _DT_TORCH[_NAME_DT[x_dtype]], (N, Ho, Wo, C), _DT_TORCH[_NAME_DT[y_dtype]],
                 (N, Ho, Wo, y_ldc))
 
@@ -356,9 +378,14 @@ def dense_plan(M, K, x_dtype, x_scale, x_zp, w: torch.Tensor, w_scale, w_zp, bia
     y_ldc = Nd if y_ldc is None else y_ldc
     xq, wq, yq = _Q(x_scale, x_zp, 1), _per_tensor_or_channel(w_scale, w_zp), _Q(y_scale, y_zp, 1)
     h = ctypes.c_void_p()
-    _check(lib().qnn_dense_plan_create(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], M, K, xq.q, _ptr(w),
-                                       Nd, wq.q, _ptr(bias), _NAME_DT[y_dtype], yq.q, _clamp(act),
-                                       _ROUND[rounding], y_ldc))
+    if w.dtype == torch.uint8:
+        _check(lib().qnn_dense_plan_create_wt(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], M, K, xq.q,
+                                              _ptr(w), UINT8, Nd, wq.q, _ptr(bias), _NAME_DT[y_dtype], yq.q,
+                                              _clamp(act), _ROUND[rounding], y_ldc))
+    else:
+        _check(lib().qnn_dense_plan_create(ctypes.byref(h), _stream(stream), _NAME_DT[x_dtype], M, K, xq.q, _ptr(w),
+                                           Nd, wq.q, _ptr(bias), _NAME_DT[y_dtype], yq.q, _clamp(act),
+                                           _ROUND[rounding], y_ldc))
     return Plan(h, (M, K), _DT_TORCH[_NAME_DT[x_dtype]], (M, Nd), _DT_TORCH[_NAME_DT[y_dtype]], (M, y_ldc))
 
 

@@ -145,14 +145,17 @@ def dense_case(layer: DenseLayer, seed: int, yt: str = "i8", zp_y: int = -3) -> 
 def conv_case(layer: ConvLayer, N: int, seed: int, *, act: Optional[str] = "auto",
               bias: bool = True, w_sigma: float = 30.0, zp_w: str = "zero",
               x_dtype: str = "u8", yt: str = "u8", rounding: str = "half_up",
-              out_q: Optional[Tuple[float, int]] = None) -> ConvCase:
+              out_q: Optional[Tuple[float, int]] = None, w_dtype: str = "i8") -> ConvCase:
     """Conv / depthwise layer with asymmetric uint8 activations (random zp),
     per-channel int8 weights rint(normal(0, w_sigma)) clipped, random output
     zero point, and a ReLU clamp on layers followed by one.
 
     zp_w: "zero" (symmetric weights), "tensor" (one zp in [-20, 20]) or
     "channel" (per-channel zps in [-20, 20]).  out_q fixes (s_y, zp_y), e.g.
-    the common output quantization of a concat group."""
+    the common output quantization of a concat group.  w_dtype "u8": asymmetric
+    uint8 weights instead, zero points in [96, 160] (per tensor for zp_w
+    "tensor", else per channel) and weights rint(normal(zp, w_sigma)) clipped
+    to [0, 255]."""
     rng = np.random.default_rng(seed)
     if x_dtype == "u8":
         x = rng.integers(0, 256, size=(N, layer.H, layer.W, layer.Cin), dtype=np.uint8)
@@ -168,7 +171,12 @@ def conv_case(layer: ConvLayer, N: int, seed: int, *, act: Optional[str] = "auto
     zp_x = int(rng.integers(lo, hi + 1))
     s_x = 0.02
     s_w = _loguniform(rng, K)
-    if zp_w == "zero":
+    if w_dtype == "u8":
+        zpw = (np.full(K, int(rng.integers(96, 161)), np.int32) if zp_w == "tensor"
+               else rng.integers(96, 161, size=K).astype(np.int32))
+        zc = zpw[None, None, :] if layer.depthwise else zpw[:, None, None, None]
+        w = np.clip(np.rint(rng.normal(0.0, w_sigma, size=w.shape)) + zc, 0, 255).astype(np.uint8)
+    elif zp_w == "zero":
         zpw = np.zeros(K, np.int32)
     elif zp_w == "tensor":
         zpw = np.full(K, int(rng.integers(-20, 21)), np.int32)
