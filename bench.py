@@ -13,11 +13,15 @@ dominant kernel, and the CPU oracle timed on a bounded sample.
 
 Other workloads (--workload): mobilenet_v2_b64, inception_v3_b64, dense_bert,
 conv14x14x64 -- the same measurement on those layer sets (depthwise layers
-and adds are reported in GB/s in the per-layer file); resnet50_b32_chain --
-ResNet-50's conv body chained as in the network (each step reads the int8
-tensor its producer wrote: the stem, its max pool, the 16 bottleneck blocks
+and adds are reported in GB/s in the per-layer file).  Chained networks,
+each step reading the int8 tensor its producer wrote, TOP/s over the convs'
+MACs and the whole chain's time: resnet50_b32_chain / resnet50_b1_chain
+(ResNet-50's conv body: the stem, its max pool, the 16 bottleneck blocks
 with a qnn.add closing each, the global average pool; 53 convs, 16 adds, 2
-pools), TOP/s over the convs' MACs and the whole chain's time.
+pools), mobilenet_v2_b64_chain / mobilenet_v2_b1_chain (the 17 inverted
+residuals: 51 convs incl. 17 depthwise, 10 adds),
+inception_v3_mixed5_b64_chain / inception_v3_mixed5_b1_chain (Mixed 5b and
+5c: 14 convs, 2 average pools, channel concats).
 """
 import argparse
 import json
@@ -95,14 +99,26 @@ class Item:
     pass
 
 
-def setup_chain(N):
-    """Plans and device tensors of the chained ResNet-50 conv body: every
-    step writes its own output tensor, which its consumers read."""
+CHAINS = {
+    "resnet50_b32_chain": ("resnet50_chain", 32),
+    "resnet50_b1_chain": ("resnet50_chain", 1),
+    "mobilenet_v2_b64_chain": ("mobilenet_v2_chain", 64),
+    "mobilenet_v2_b1_chain": ("mobilenet_v2_chain", 1),
+    "inception_v3_mixed5_b64_chain": ("inception_v3_mixed5_chain", 64),
+    "inception_v3_mixed5_b1_chain": ("inception_v3_mixed5_chain", 1),
+}
+
+
+def setup_chain(workload):
+    """Plans and device tensors of a chained network: every step writes its
+    own output tensor (or its channel slice of a concat), which its
+    consumers read."""
     import torch
     import workloads as W
     from paper_2006_10226_amd import qnn as Q
 
-    ch = W.resnet50_chain(N)
+    fn, N = CHAINS[workload]
+    ch = getattr(W, fn)(N)
     t = {"x0": torch.from_numpy(ch.x0).cuda()}
     items = []
     for st in ch.steps:
@@ -112,14 +128,24 @@ def setup_chain(N):
             s_x, zp_x = ch.q[st.src]
             it.kind, it.layer, it.name = "conv", L, L.name
             it.w, it.bias = torch.from_numpy(st.w).cuda(), torch.from_numpy(st.bias).cuda()
-            it.plan = Q.conv2d_plan(tuple(t[st.src].shape), "i8", s_x, zp_x, it.w, st.s_w, st.zp_w, it.bias,
-                                    L.stride, L.pads, 1, st.s_y, st.zp_y, "i8", st.act)
+            shape = tuple(t[st.src].shape)
+            if L.depthwise:
+                it.kind = "dw"
+                it.plan = Q.depthwise_conv2d_plan(shape, "i8", s_x, zp_x, it.w, st.s_w, st.zp_w, it.bias, L.stride,
+                                                  L.pads, 1, st.s_y, st.zp_y, "i8", st.act)
+            else:
+                off, total = st.y_off if st.y_off is not None else (0, None)
+                it.plan = Q.conv2d_plan(shape, "i8", s_x, zp_x, it.w, st.s_w, st.zp_w, it.bias,
+                                        L.stride, L.pads, 1, st.s_y, st.zp_y, "i8", st.act, y_ldc=total, y_coff=off)
             it.x = t[st.src]
-            it.out = t[st.dst] = it.plan.new_output()
+            if st.y_off is not None and st.dst in t:
+                it.out = t[st.dst]   # another branch's slice of the same concat
+            else:
+                it.out = t[st.dst] = it.plan.new_output()
             it.desc = it.plan.describe()
             Nb, Ho, Wo, K = it.plan.out_shape
-            it.macs = Nb * Ho * Wo * K * L.R * L.S * L.Cin
-            it.bytes = it.x.numel() + st.w.size + it.out.numel()
+            it.macs = Nb * Ho * Wo * K * L.R * L.S * (1 if L.depthwise else L.Cin)
+            it.bytes = it.x.numel() + st.w.size + Nb * Ho * Wo * K
             it.run = (lambda it=it: it.plan.run(it.x, it.out))
         elif isinstance(st, W.ChainPool):
             it.kind, it.layer, it.name, it.desc = "pool", None, st.name, "pool"
@@ -146,8 +172,8 @@ def setup(workload):
     import torch
     from paper_2006_10226_amd import qnn as Q
 
-    if workload == "resnet50_b32_chain":
-        return setup_chain(32)
+    if workload in CHAINS:
+        return setup_chain(workload)
     layers, batch = _layers(workload)
     items = []
     for kind, layer, c in layers:
@@ -282,9 +308,12 @@ def cpu_baseline(workload, target_s=12.0):
     from oracle import oracle as O
     import workloads as W
 
-    if workload == "resnet50_b32_chain":
+    if workload in CHAINS:
         # the chain's conv shapes, sampled on independent seeded inputs
-        layers, _ = _layers("resnet50_b32")
+        fn, N = CHAINS[workload]
+        ch = getattr(W, fn)(N)
+        layers = [("dw" if st.layer.depthwise else "conv", st.layer, W.conv_case(st.layer, N, seed=7000 + i))
+                  for i, st in enumerate(ch.steps) if isinstance(st, W.ChainConv)]
     else:
         layers, _ = _layers(workload)
     convs = [(k, l, c) for k, l, c in layers if k in ("conv", "dense", "dw")]

@@ -1,7 +1,11 @@
-"""ResNet-50's conv body chained as in the network (stem, max pool, the 16
-bottleneck blocks with int8 hand-off and a qnn.add closing every block,
-global average pool) on the GPU against the oracle running the same chain on
-its own tensors: every one of the 71 intermediate tensors byte for byte."""
+"""Networks chained as they run, on the GPU against the oracle running the
+same chain on its own tensors, every intermediate tensor byte for byte:
+ResNet-50's conv body (stem, max pool, the 16 bottleneck blocks with int8
+hand-off and a qnn.add closing every block, global average pool: 71
+steps); MobileNet-V2's 17 expansion-6 inverted residuals (1x1 expand,
+depthwise 3x3, 1x1 project, residual qnn.add: 58 steps); Inception-v3's
+Mixed 5b and 5c (four branches, average-pool branch, channel concat with
+the block's common quantization: 16 steps)."""
 import numpy as np
 import pytest
 import torch
@@ -25,9 +29,19 @@ def run_chain_gpu(ch):
             L = st.layer
             w, b = dev(st.w), dev(st.bias)
             keep += [w, b]
-            p = Q.conv2d_plan(tuple(t[st.src].shape), "i8", s_x, zp_x, w, st.s_w, st.zp_w, b, L.stride, L.pads,
-                              1, st.s_y, st.zp_y, "i8", st.act)
-            out = p.new_output()
+            shape = tuple(t[st.src].shape)
+            if L.depthwise:
+                p = Q.depthwise_conv2d_plan(shape, "i8", s_x, zp_x, w, st.s_w, st.zp_w, b, L.stride, L.pads, 1,
+                                            st.s_y, st.zp_y, "i8", st.act)
+            elif st.y_off is not None:
+                p = Q.conv2d_plan(shape, "i8", s_x, zp_x, w, st.s_w, st.zp_w, b, L.stride, L.pads, 1, st.s_y,
+                                  st.zp_y, "i8", st.act, y_ldc=st.y_off[1], y_coff=st.y_off[0])
+            else:
+                p = Q.conv2d_plan(shape, "i8", s_x, zp_x, w, st.s_w, st.zp_w, b, L.stride, L.pads,
+                                  1, st.s_y, st.zp_y, "i8", st.act)
+            if st.y_off is not None and st.dst not in t:
+                t[st.dst] = torch.full(p.y_ldc_shape, 77, dtype=torch.int8, device="cuda")
+            out = t[st.dst] if st.y_off is not None else p.new_output()
             p.run(t[st.src], out)
             torch.cuda.synchronize()
             p.close()
@@ -48,8 +62,15 @@ def run_chain_oracle(ch):
         if isinstance(st, W.ChainConv):
             s_x, zp_x = ch.q[st.src]
             L = st.layer
-            t[st.dst] = O.conv2d(t[st.src], s_x, zp_x, st.w, st.s_w, st.zp_w, st.bias, st.s_y, st.zp_y, "i8",
-                                 st.act, "half_up", stride=(L.stride, L.stride), pads=L.pads)
+            y = O.conv2d(t[st.src], s_x, zp_x, st.w, st.s_w, st.zp_w, st.bias, st.s_y, st.zp_y, "i8",
+                         st.act, "half_up", stride=(L.stride, L.stride), pads=L.pads, depthwise=L.depthwise)
+            if st.y_off is None:
+                t[st.dst] = y
+            else:
+                off, total = st.y_off
+                if st.dst not in t:
+                    t[st.dst] = np.full(y.shape[:3] + (total,), 77, np.int8)
+                t[st.dst][..., off:off + y.shape[3]] = y
         elif isinstance(st, W.ChainPool):
             t[st.dst] = O.pool2d(t[st.src], st.mode, st.kernel, st.stride, st.pads)
         else:
@@ -72,3 +93,30 @@ def test_resnet50_chain(N):
     # and the pooled features are neither constant nor all on the clamp
     assert len(np.unique(ref[ch.steps[-2].dst])) > 50
     assert len(np.unique(ref["gap"])) > 20
+
+
+@pytest.mark.parametrize("N", [1, 2])
+def test_mobilenet_v2_chain(N):
+    ch = W.mobilenet_v2_chain(N)
+    log(f"mobilenet chain N={N}: {len(ch.steps)} steps")
+    gpu = run_chain_gpu(ch)
+    ref = run_chain_oracle(ch)
+    for st in ch.steps:
+        assert_equal(gpu[st.dst], ref[st.dst], f"mobilenet chain N={N} {st.dst}")
+    assert len(ch.steps) == 58 and ref[ch.steps[-1].dst].shape == (N, 7, 7, 320)
+    assert len(np.unique(ref[ch.steps[-1].dst])) > 50
+
+
+@pytest.mark.parametrize("N", [1, 2])
+def test_inception_mixed5_chain(N):
+    ch = W.inception_v3_mixed5_chain(N)
+    log(f"inception mixed chain N={N}: {len(ch.steps)} steps")
+    gpu = run_chain_gpu(ch)
+    ref = run_chain_oracle(ch)
+    for st in ch.steps:
+        assert_equal(gpu[st.dst], ref[st.dst], f"inception chain N={N} {st.dst}")
+    # every channel of both concats was written by a branch (no sentinel left)
+    for g, total in (("mixed5b", 256), ("mixed5c", 288)):
+        assert ref[g].shape == (N, 35, 35, total)
+        assert not (gpu[g] == 77).all(axis=(0, 1, 2)).any(), g
+    assert len(np.unique(ref["mixed5c"])) > 50

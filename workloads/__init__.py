@@ -7,4 +7,5 @@ from .shapes import (ConvLayer, DenseLayer, AddLayer, InvertedResidual, resnet50
                      SINGLE_CONV)
 from .generate import (ConvCase, AddCase, single_conv_case, dense_case, conv_case,
                        add_case, sample_indices)
-from .chain import Chain, ChainConv, ChainAdd, ChainPool, resnet50_chain
+from .chain import (Chain, ChainConv, ChainAdd, ChainPool, resnet50_chain, mobilenet_v2_chain,
+                    inception_v3_mixed5_chain)
