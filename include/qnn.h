@@ -57,7 +57,16 @@ extern "C" {
 
 #define QNN_ABI_VERSION 1
 
-typedef enum {
+/* The enums are int-sized in C.  In C++ they get int as their fixed
+ * underlying type, so that every int a caller passes is a value of the
+ * enum type (the library validates it) rather than an out-of-range one. */
+#ifdef __cplusplus
+#define QNN_ENUM_INT : int
+#else
+#define QNN_ENUM_INT
+#endif
+
+typedef enum QNN_ENUM_INT {
     QNN_OK = 0,
     QNN_ERR_NULL = 1,        /* a required pointer is NULL */
     QNN_ERR_SHAPE = 2,       /* non-positive or inconsistent sizes, bad y_ldc/y_coff */
@@ -69,7 +78,7 @@ typedef enum {
     QNN_ERR_ALLOC = 8        /* device or host allocation failed */
 } qnn_status;
 
-typedef enum { QNN_UINT8 = 0, QNN_INT8 = 1, QNN_INT32 = 2 } qnn_dtype;
+typedef enum QNN_ENUM_INT { QNN_UINT8 = 0, QNN_INT8 = 1, QNN_INT32 = 2 } qnn_dtype;
 
 /* Rounding of the fixed-point requantize (the paper leaves it to the
  * framework, Sec. III-B): HALF_UP rounds round(v * mult / 2^shift) with ties
@@ -79,7 +88,7 @@ typedef enum { QNN_UINT8 = 0, QNN_INT8 = 1, QNN_INT32 = 2 } qnn_dtype;
  * integer by 2^(shift - 31) rounding half away from zero (two roundings,
  * so a result may differ by 1 from either single rounding); for shift < 31
  * (multipliers of 1 or more) one half-up rounding. */
-typedef enum { QNN_ROUND_HALF_UP = 0, QNN_ROUND_HALF_AWAY = 1, QNN_ROUND_TWO_STAGE = 2 } qnn_rounding;
+typedef enum QNN_ENUM_INT { QNN_ROUND_HALF_UP = 0, QNN_ROUND_HALF_AWAY = 1, QNN_ROUND_TWO_STAGE = 2 } qnn_rounding;
 
 /* Quantization attributes of one tensor (host arrays).  n == 1: per tensor;
  * n == channel count: per output channel (weights) or per innermost channel
@@ -221,7 +230,7 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
                    void *y, qnn_dtype y_dtype, qnn_qparams y_q, qnn_clamp act,
                    qnn_rounding rounding);
 
-typedef enum {
+typedef enum QNN_ENUM_INT {
     QNN_POOL_AVG = 0,
     QNN_POOL_MAX = 1
 } qnn_pool_mode;
