@@ -278,9 +278,11 @@ def time_launches(items, steps):
     kernels run on (torch's current stream).  A layer with a plan runs through
     qnn_plan_run_timed, whose main kernel records the two events at its own
     start and end (hipExtLaunchKernel): its duration as rocprofv3 reports it.
-    Other steps (adds, pools) are bracketed by events around the call, which
-    also times the dispatch gaps.  Returns (median ms per item, how)."""
+    Other steps (adds, pools) ask the library to have their kernel record
+    the events the same way (qnn_time_next_kernel).  Returns (median ms per
+    item, how it was timed)."""
     import torch
+    from paper_2006_10226_amd import qnn as Q
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in items]
           for _ in range(steps)]
     torch.cuda.synchronize()
@@ -290,14 +292,11 @@ def time_launches(items, steps):
             if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw"):
                 it.plan.run_timed(it.x, it.out, getattr(it, "ws", None), a, b)
             else:
-                a.record()
+                Q.time_next_kernel(a, b)   # the add's or pool's own kernel records them
                 it.run()
-                b.record()
     torch.cuda.synchronize()
     per = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # ms
-    how = ["kernel" if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw") else "bracketed"
-           for it in items]
-    return np.median(per, axis=0), how
+    return np.median(per, axis=0), ["kernel"] * len(items)
 
 
 # ------------------------------------------------------------------ CPU oracle baseline

@@ -365,6 +365,15 @@ qnn_status qnn_plan_run_timed(const qnn_plan *plan, void *stream, const void *x,
                               void *start_event, void *stop_event);
 
 /*
+ * For measurement of the one-shot calls (qnn_add, qnn_requantize,
+ * qnn_pool2d, ...): the next main kernel that this host thread launches
+ * through an entry point records start_event and stop_event (hipEvent_t as
+ * void*) at its own start and end, as qnn_plan_run_timed does.  NULL for
+ * either event cancels a pending request.  Always returns QNN_OK.
+ */
+qnn_status qnn_time_next_kernel(void *start_event, void *stop_event);
+
+/*
  * Allocation-free run, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): runs the plan like qnn_plan_run, with its workspace taken from

@@ -331,7 +331,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
             const uint32_t packed = requant4(a, v, rec);
             uint8_t *yp = (uint8_t *)a.y + off;
             if (full) {
-                *(uint32_t *)yp = packed;
+                __builtin_nontemporal_store(packed, (uint32_t *)yp);
             } else {
                 for (int e = 0; e < 4 && ch + e < a.K; ++e)
                     yp[e] = (uint8_t)(packed >> (8 * e));
@@ -351,7 +351,7 @@ __global__ void __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) conv_halo_kernel(Con
         const v4i v = *(const v4i *)(stage + pl * kStagePitch + qc * 16);
         uint8_t *dst = (uint8_t *)a.y + (size_t)(m0 + pl) * a.y_ldc + a.y_coff + c0 + qc * 16;
         if (qc * 16 + 16 <= kmax) {
-            *(v4i *)dst = v;
+            __builtin_nontemporal_store(v, (v4i *)dst);
         } else {
             for (int e = 0; e < kmax - qc * 16; ++e)
                 dst[e] = (uint8_t)((uint32_t)v[e >> 2] >> (8 * (e & 3)));

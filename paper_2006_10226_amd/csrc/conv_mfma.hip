@@ -374,7 +374,7 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
                 }
                 uint8_t *yp = (uint8_t *)a.y + off;
                 if (full) {
-                    *(uint32_t *)yp = packed;
+                    __builtin_nontemporal_store(packed, (uint32_t *)yp);
                 } else {
                     for (int e = 0; e < 4 && ch + e < a.K; ++e)
                         yp[e] = (uint8_t)(packed >> (8 * e));
@@ -458,7 +458,7 @@ __global__ void __launch_bounds__(256, ((TC + TP) * BK * 2 <= 80 * 1024) ? 2 : 1
                     const v4i v = *(const v4i *)(stage + pl * SP + qc * 16);
                     uint8_t *dst = (uint8_t *)a.y + (size_t)m * a.y_ldc + a.y_coff + c0 + qc * 16;
                     if (qc * 16 + 16 <= kmax) {
-                        *(v4i *)dst = v;
+                        __builtin_nontemporal_store(v, (v4i *)dst);
                     } else {
                         for (int e = 0; e < kmax - qc * 16; ++e) {
                             const int w = e < 4 ? v.x : e < 8 ? v.y : e < 12 ? v.z : v.w;

@@ -399,7 +399,7 @@ __global__ void __launch_bounds__(NB * KS * 64, 1) conv_window_kernel(ConvArgs a
             if (a.mode == OUT_INT32) {
                 int32_t *yp = (int32_t *)a.y + off;
                 if (full) {
-                    *(v4i *)yp = v;
+                    __builtin_nontemporal_store(v, (v4i *)yp);
                 } else {
                     for (int e = 0; e < 4 && ch + e < a.K; ++e)
                         yp[e] = v[e];
@@ -408,7 +408,7 @@ __global__ void __launch_bounds__(NB * KS * 64, 1) conv_window_kernel(ConvArgs a
                 const uint32_t packed = requant4(a, v, rec);
                 uint8_t *yp = (uint8_t *)a.y + off;
                 if (full) {
-                    *(uint32_t *)yp = packed;
+                    __builtin_nontemporal_store(packed, (uint32_t *)yp);
                 } else {
                     for (int e = 0; e < 4 && ch + e < a.K; ++e)
                         yp[e] = (uint8_t)(packed >> (8 * e));
@@ -429,7 +429,7 @@ __global__ void __launch_bounds__(NB * KS * 64, 1) conv_window_kernel(ConvArgs a
         const v4i v = *(const v4i *)(stage + pl * SP + qc * 16);
         uint8_t *dst = (uint8_t *)a.y + (size_t)(m0 + pl) * a.y_ldc + a.y_coff + c0 + qc * 16;
         if (qc * 16 + 16 <= kmax) {
-            *(v4i *)dst = v;
+            __builtin_nontemporal_store(v, (v4i *)dst);
         } else {
             for (int e = 0; e < kmax - qc * 16; ++e)
                 dst[e] = (uint8_t)((uint32_t)v[e >> 2] >> (8 * (e & 3)));

@@ -36,6 +36,10 @@ __device__ __forceinline__ int dot4(uint32_t a, uint32_t b, int c)
     return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
+// cache policy of the output stores: nt, the streaming hint (the output is
+// written once; it need not stay in this XCD's L2)
+constexpr int kStream = 2;
+
 // byte selector of v_perm_b32: 0..3 bytes of `lo`, 4..7 bytes of `hi`,
 // 12 a zero byte
 constexpr uint32_t kZero = 0x0c;
@@ -158,7 +162,7 @@ __global__ void __launch_bounds__(256) depthwise3_kernel(DwArgs a)
             const int off = (m * a.y_ldc + a.y_coff + c0) * 4;
 #pragma unroll
             for (int c = 0; c < 8; ++c)
-                __builtin_amdgcn_raw_buffer_store_b32(v[c], ry, off + 4 * c, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(v[c], ry, off + 4 * c, 0, kStream);
             continue;
         }
         uint32_t packed[2] = {0u, 0u};
@@ -184,11 +188,12 @@ __global__ void __launch_bounds__(256) depthwise3_kernel(DwArgs a)
         if (a.vec_store) {
             __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) unsigned,
                                                                      uint2{packed[0], packed[1]}),
-                                                  ry, off, 0, 0);
+                                                  ry, off, 0, kStream);
         } else {
 #pragma unroll
             for (int c = 0; c < 8; ++c)
-                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(packed[c >> 2] >> (8 * (c & 3))), ry, off + c, 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(packed[c >> 2] >> (8 * (c & 3))), ry, off + c, 0,
+                                                     kStream);
         }
     }
 }

@@ -15,6 +15,8 @@
 
 namespace qnn {
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ int clampll(long long v, int lo, int hi)
 {
     return (int)(v < lo ? lo : (v > hi ? hi : v));
@@ -167,13 +169,13 @@ __device__ __forceinline__ void st16(void *p, long long i0, const int v[16])
         int4 *q = (int4 *)((int32_t *)p + i0);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            q[k] = make_int4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
+            __builtin_nontemporal_store(v4i{v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]}, (v4i *)(q + k));
     } else {
         uint32_t w[4] = {0, 0, 0, 0};
 #pragma unroll
         for (int k = 0; k < 16; ++k)
             w[k >> 2] |= ((uint32_t)v[k] & 0xffu) << (8 * (k & 3));
-        *(int4 *)((uint8_t *)p + i0) = make_int4(w[0], w[1], w[2], w[3]);
+        __builtin_nontemporal_store(v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]}, (v4i *)((uint8_t *)p + i0));
     }
 }
 
@@ -275,8 +277,8 @@ static dim3 ew_grid(long long count)
 template <int XDT, int YDT>
 static void req_launch(const ReqArgs &a, bool vec, hipStream_t s)
 {
-    if (vec) hipLaunchKernelGGL((requantize_kernel<XDT, YDT, true>), ew_grid(a.count), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((requantize_kernel<XDT, YDT, false>), ew_grid(a.count), dim3(256), 0, s, a);
+    if (vec) launch_main((requantize_kernel<XDT, YDT, true>), ew_grid(a.count), dim3(256), 0, s, a);
+    else launch_main((requantize_kernel<XDT, YDT, false>), ew_grid(a.count), dim3(256), 0, s, a);
 }
 
 template <int XDT>
@@ -298,8 +300,8 @@ hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, h
 template <int ADT, int BDT, int YDT>
 static void add_launch(const AddArgs &a, bool vec, hipStream_t s)
 {
-    if (vec) hipLaunchKernelGGL((add_kernel<ADT, BDT, YDT, true>), ew_grid(a.count), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((add_kernel<ADT, BDT, YDT, false>), ew_grid(a.count), dim3(256), 0, s, a);
+    if (vec) launch_main((add_kernel<ADT, BDT, YDT, true>), ew_grid(a.count), dim3(256), 0, s, a);
+    else launch_main((add_kernel<ADT, BDT, YDT, false>), ew_grid(a.count), dim3(256), 0, s, a);
 }
 
 template <int ADT, int BDT>

@@ -136,12 +136,14 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
         for (int i = 0; i < V; ++i)
             o[i / 4] |= ((unsigned)acc[i] & 0xffu) << (8 * (i % 4));
         int8_t *dst = (int8_t *)a.y + (size_t)u * V;
-        if constexpr (V == 16)
-            *(uint4 *)dst = make_uint4(o[0], o[1], o[2], o[3]);
-        else if constexpr (V == 4)
-            *(unsigned *)dst = o[0];
-        else
+        if constexpr (V == 16) {
+            typedef unsigned u4 __attribute__((ext_vector_type(4)));
+            __builtin_nontemporal_store(u4{o[0], o[1], o[2], o[3]}, (u4 *)dst);
+        } else if constexpr (V == 4) {
+            __builtin_nontemporal_store(o[0], (unsigned *)dst);
+        } else {
             *dst = (int8_t)(o[0] & 0xffu);
+        }
     }
 }
 
@@ -222,7 +224,7 @@ __global__ void __launch_bounds__(64 * SPLIT_WAVES) pool_split_kernel(PoolArgs a
     for (int i = 0; i < V; ++i)
         o |= ((unsigned)acc[i] & 0xffu) << (8 * i);
     if constexpr (V == 4)
-        *(unsigned *)dst = o;
+        __builtin_nontemporal_store(o, (unsigned *)dst);
     else
         *dst = (int8_t)(o & 0xffu);
 }
@@ -232,8 +234,8 @@ static void launch_split_t(const PoolArgs &a, int vec, hipStream_t s)
 {
     const int chunks = (a.C / vec + 63) / 64;
     const dim3 grid((unsigned)((long long)a.N * a.Ho * a.Wo * chunks));
-    if (vec == 4) hipLaunchKernelGGL((pool_split_kernel<SIGNED, MAX, 4>), grid, dim3(64 * SPLIT_WAVES), 0, s, a, chunks);
-    else hipLaunchKernelGGL((pool_split_kernel<SIGNED, MAX, 1>), grid, dim3(64 * SPLIT_WAVES), 0, s, a, chunks);
+    if (vec == 4) launch_main((pool_split_kernel<SIGNED, MAX, 4>), grid, dim3(64 * SPLIT_WAVES), 0, s, a, chunks);
+    else launch_main((pool_split_kernel<SIGNED, MAX, 1>), grid, dim3(64 * SPLIT_WAVES), 0, s, a, chunks);
 }
 
 hipError_t launch_pool_split(const PoolArgs &a, bool is_signed, int vec, hipStream_t s)
@@ -255,11 +257,11 @@ template <bool SIGNED, bool MAX>
 static void launch_pool_t(const PoolArgs &a, int vec, dim3 grid, hipStream_t s)
 {
     const bool pack = !MAX && (long long)a.R * a.S <= 257;
-    if (vec == 16 && pack) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 16, !MAX>), grid, dim3(256), 0, s, a);
-    else if (vec == 16) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 16>), grid, dim3(256), 0, s, a);
-    else if (vec == 4 && pack) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 4, !MAX>), grid, dim3(256), 0, s, a);
-    else if (vec == 4) hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 4>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((pool_kernel<SIGNED, MAX, 1>), grid, dim3(256), 0, s, a);
+    if (vec == 16 && pack) launch_main((pool_kernel<SIGNED, MAX, 16, !MAX>), grid, dim3(256), 0, s, a);
+    else if (vec == 16) launch_main((pool_kernel<SIGNED, MAX, 16>), grid, dim3(256), 0, s, a);
+    else if (vec == 4 && pack) launch_main((pool_kernel<SIGNED, MAX, 4, !MAX>), grid, dim3(256), 0, s, a);
+    else if (vec == 4) launch_main((pool_kernel<SIGNED, MAX, 4>), grid, dim3(256), 0, s, a);
+    else launch_main((pool_kernel<SIGNED, MAX, 1>), grid, dim3(256), 0, s, a);
 }
 
 hipError_t launch_pool(const PoolArgs &a, bool is_signed, int vec, hipStream_t s)

@@ -1802,6 +1802,16 @@ qnn_status qnn_plan_run_timed(const qnn_plan *plan, void *stream, const void *x,
     return s;
 }
 
+qnn_status qnn_time_next_kernel(void *start_event, void *stop_event)
+{
+    LaunchEvents &ev = launch_events();
+    ev.start = (hipEvent_t)start_event;
+    ev.stop = (hipEvent_t)stop_event;
+    if (!start_event || !stop_event)
+        ev = LaunchEvents{};
+    return QNN_OK;
+}
+
 qnn_status qnn_plan_run_noalloc(const qnn_plan *plan, void *stream, const void *x, void *y)
 {
     if (!plan)

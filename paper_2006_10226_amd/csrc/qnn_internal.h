@@ -8,25 +8,28 @@
 
 namespace qnn {
 
-// Events that the main kernel of the next plan run records at its own
-// start and end (qnn_plan_run_timed), null when nothing is measured; one
-// pair per host thread.
+// Events that the next main kernel this host thread launches records at its
+// own start and end (qnn_plan_run_timed, qnn_time_next_kernel), null when
+// nothing is measured.
 struct LaunchEvents {
     hipEvent_t start = nullptr, stop = nullptr;
 };
 LaunchEvents &launch_events();
 
-// Launch of a plan's main kernel: with timing events set, through
-// hipExtLaunchKernel, which records them at the kernel's own start and end
-// (the dispatch itself, as the profiler times it), else a plain launch.
+// Launch of an operator's main kernel (conv, dense, depthwise, requantize,
+// add, pool): with timing events set, through hipExtLaunchKernel, which
+// records them at the kernel's own start and end (the dispatch itself, as
+// the profiler times it) and consumes them; else a plain launch.
 template <typename K, typename... A>
 inline void launch_main(K kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st, A... args)
 {
-    const LaunchEvents &ev = launch_events();
-    if (ev.start)
+    LaunchEvents &ev = launch_events();
+    if (ev.start) {
         hipExtLaunchKernelGGL(kernel, grid, block, lds, st, ev.start, ev.stop, 0, args...);
-    else
+        ev = LaunchEvents{};
+    } else {
         kernel<<<grid, block, lds, st>>>(args...);
+    }
 }
 
 // Per-output-channel epilogue record of a conv / dense plan.

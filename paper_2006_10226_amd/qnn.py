@@ -40,7 +40,7 @@ EXPORTS = [
     "qnn_pool2d",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
     "qnn_conv2d_plan_create_wt", "qnn_depthwise_conv2d_plan_create_wt", "qnn_dense_plan_create_wt",
-    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_timed", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
+    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_timed", "qnn_time_next_kernel", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
     "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
 ]
 
@@ -126,6 +126,8 @@ def lib() -> ctypes.CDLL:
     L.qnn_plan_run.restype = st
     L.qnn_plan_run_timed.argtypes = [P, P, P, P, P, P, P]
     L.qnn_plan_run_timed.restype = st
+    L.qnn_time_next_kernel.argtypes = [P, P]
+    L.qnn_time_next_kernel.restype = st
     L.qnn_plan_run_noalloc.argtypes = [P, P, P, P]
     L.qnn_plan_run_noalloc.restype = st
     L.qnn_plan_workspace_size.argtypes = [P]
@@ -223,6 +225,15 @@ def quantize_multiplier(M: float) -> Tuple[int, int]:
     m, s = ctypes.c_int32(), ctypes.c_int32()
     _check(lib().qnn_quantize_multiplier(float(M), ctypes.byref(m), ctypes.byref(s)))
     return m.value, s.value
+
+
+def time_next_kernel(start, stop):
+    """The next main kernel launched from this thread records the two
+    torch.cuda.Event objects at its own start and end."""
+    for e in (start, stop):
+        if not e.cuda_event:   # torch creates its events on first record
+            e.record()
+    _check(lib().qnn_time_next_kernel(ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event)))
 
 
 def set_tuning_file(path: Optional[str]):
