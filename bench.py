@@ -270,7 +270,7 @@ def time_steps(items, steps, warmup, use_graph):
                 it.run()
     end.record()
     torch.cuda.synchronize()
-    return start.elapsed_time(end) / steps, graph is not None
+    return start.elapsed_time(end) / steps, graph
 
 
 def time_launches(items, steps):
@@ -297,6 +297,75 @@ def time_launches(items, steps):
     torch.cuda.synchronize()
     per = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # ms
     return np.median(per, axis=0), ["kernel"] * len(items)
+
+
+def time_warm(items, reps=10):
+    """Per-layer kernel time with the layer's inputs, weights and output
+    already in the caches: each layer runs `reps` times back to back (after
+    two untimed runs), timed by its own kernel's events as in
+    time_launches.  Returns the median ms per item."""
+    import torch
+    from paper_2006_10226_amd import qnn as Q
+    out = []
+    for it in items:
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        it.run()
+        it.run()
+        for a, b in ev:
+            if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw"):
+                it.plan.run_timed(it.x, it.out, getattr(it, "ws", None), a, b)
+            else:
+                Q.time_next_kernel(a, b)
+                it.run()
+        torch.cuda.synchronize()
+        out.append(float(np.median([a.elapsed_time(b) for a, b in ev])))
+    return np.array(out)
+
+
+def sample_clock(items, graph_step, seconds=2.0, settle=1.0):
+    """The GPU's graphics clock while the step runs: steps run back to back
+    for `seconds` while a thread reads the current clock (amdsmi, through
+    torch.cuda.clock_rate) every 10 ms.  The reading is refreshed by the
+    driver only every 1/6 to 1 s, so only reads taken after `settle`
+    seconds of stepping count.  Kept out of the timed steps so that the
+    reads cannot slow their launches.  Returns {min, median, max, samples}
+    in MHz, or None when the clock cannot be read."""
+    import threading
+    import torch
+    try:
+        torch.cuda.clock_rate()
+    except Exception as e:   # no amdsmi on this machine: report no clock
+        log(f"GPU clock not readable ({e})")
+        return None
+    reads, stop = [], threading.Event()
+    t0 = time.perf_counter()
+
+    def poll():
+        while not stop.is_set():
+            try:
+                reads.append((time.perf_counter() - t0, int(torch.cuda.clock_rate())))
+            except Exception:
+                return
+            time.sleep(0.01)
+
+    th = threading.Thread(target=poll, daemon=True)
+    th.start()
+    try:
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(10):
+                if graph_step is not None:
+                    graph_step.replay()
+                else:
+                    for it in items:
+                        it.run()
+            torch.cuda.synchronize()
+    finally:
+        stop.set()
+        th.join()
+    mhz = [m for t, m in reads if settle <= t <= seconds]
+    if not mhz:
+        return None
+    return {"min": min(mhz), "median": int(np.median(mhz)), "max": max(mhz), "samples": len(mhz)}
 
 
 # ------------------------------------------------------------------ CPU oracle baseline
@@ -336,16 +405,42 @@ def cpu_baseline(workload, target_s=12.0):
             macs += idx.size * c.J
         return macs, time.perf_counter() - t0
 
-    # grow the sample until one pass takes about target_s of wall-clock
-    per = 16
-    while True:
-        macs, t = run(per)
-        if t >= 0.6 * target_s or per >= 4000000:
-            break
-        per = min(4000000, int(per * min(16.0, max(2.0, target_s / max(t, 1e-3)))))
-    return {"value": round(2.0 * macs / t / 1e12, 6), "unit": "TOP/s", "cores": O.threads(), "kind": "oracle",
-            "sample": f"{per} randomly chosen outputs of each of the {len(convs)} layers of the same workload "
-                      f"({macs / 1e9:.2f} G MAC in {t:.1f} s, requantize included)"}
+    def grow(target):
+        # grow the sample until one pass takes about `target` s of wall-clock
+        per = 16
+        while True:
+            macs, t = run(per)
+            if t >= 0.6 * target or per >= 4000000:
+                return per, macs, t
+            per = min(4000000, int(per * min(16.0, max(2.0, target / max(t, 1e-3)))))
+
+    def sample(per, macs, t):
+        return (f"{per} randomly chosen outputs of each of the {len(convs)} layers of the same workload "
+                f"({macs / 1e9:.2f} G MAC in {t:.1f} s, requantize included)")
+
+    cores = O.threads()
+    per, macs, t = grow(target_s)
+    # the same loops on one thread, on a smaller sample
+    O.set_threads(1)
+    try:
+        per1, macs1, t1 = grow(target_s / 3)
+    finally:
+        O.set_threads(cores)
+    return {"value": round(2.0 * macs / t / 1e12, 6), "unit": "TOP/s", "cores": cores, "kind": "oracle",
+            "sample": sample(per, macs, t),
+            "value_1_thread": round(2.0 * macs1 / t1 / 1e12, 6), "sample_1_thread": sample(per1, macs1, t1),
+            "host_cpu": host_cpu(), "nproc": os.cpu_count()}
+
+
+def host_cpu():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 # ------------------------------------------------------------------ traffic from committed counters
@@ -430,7 +525,8 @@ def main():
     total_bytes = sum(it.bytes for it in items)
     log(f"{len(items)} layers, {total_macs / 1e9:.2f} G MAC per step")
 
-    ms, graphed = time_steps(items, args.steps, args.warmup, not args.no_graph)
+    ms, graph = time_steps(items, args.steps, args.warmup, not args.no_graph)
+    graphed = graph is not None
     if graphed:
         # a graph replay has a fixed launch cost that dominates a step of
         # one or two small layers; such steps are timed as eager launches
@@ -442,6 +538,9 @@ def main():
     log(f"step {ms:.4f} ms -> {value:.1f} TOP/s (graph={graphed})")
 
     per, how = time_launches(items, args.steps)
+    warm = time_warm(items)
+    clock = sample_clock(items, graph if graphed else None)
+    log(f"GPU clock while stepping: {clock}")
     groups = {}
     for it, t in zip(items, per):
         g = kernel_group(it)
@@ -502,8 +601,9 @@ def main():
                          "ceiling_frac_of_int8_peak": round(cb_ops / (cb_roof_us * 1e-6) / 1e12 / PEAK_INT8_TOPS, 4),
                          "share_of_step": round(cb_ms / ms, 4)}
     layer_rows = []
-    for it, t, h in zip(items, per, how):
+    for it, t, h, tw in zip(items, per, how, warm):
         row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3), "timed": h,
+               "warm_us": round(float(tw) * 1e3, 3),
                "gmac": round(it.macs / 1e9, 4), "mbytes": round(it.bytes / 1e6, 3)}
         if it.macs:
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
@@ -549,7 +649,12 @@ def main():
                    # the best the stack could reach: every layer at its own roofline
                    "stack_ceiling_frac_of_int8_peak": round(2.0 * total_macs / (roof_us * 1e-6) / 1e12
                                                             / PEAK_INT8_TOPS, 4),
-                   "compute_bound_layers": compute_bound},
+                   "compute_bound_layers": compute_bound,
+                   # kernel times summed over the layers: cold (inside the step, each layer's
+                   # inputs last touched a step earlier) and warm (each layer repeated back to back)
+                   "layer_kernel_sum_us": {"cold": round(float(np.sum(per)) * 1e3, 2),
+                                           "warm": round(float(np.sum(warm)) * 1e3, 2)},
+                   "gpu_clock_mhz": clock},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -75,6 +75,8 @@ def _load():
                                i64, i64, i32, P]
     lib.oracle_add.restype = ctypes.c_int
     lib.oracle_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = None
     _lib = lib
     return lib
 
@@ -82,6 +84,11 @@ def _load():
 def threads() -> int:
     """OpenMP threads the oracle's loops run on."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Run the oracle's later loops on n threads (timing only)."""
+    _load().oracle_set_threads(int(n))
 
 
 def _ptr(a):

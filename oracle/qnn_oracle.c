@@ -537,6 +537,14 @@ int oracle_requantize_value(int64_t v, double M, int32_t zp_out, int32_t yt,
     return requantize_one(v, M, zp_out, yt, lo, hi, rounding, out);
 }
 
+/* Thread count for the oracle's later parallel loops (n >= 1); timing
+   only, the results do not depend on it. */
+void oracle_set_threads(int n)
+{
+    if (n >= 1)
+        omp_set_num_threads(n);
+}
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int oracle_threads(void)
 {
