@@ -697,6 +697,182 @@ int device_cus()
 // tune: time the candidate kernels when the kernel-choice records hold no
 // choice for this shape (plans); one-shot calls pass false and take the
 // recorded choice or else the first candidate, without timing.
+// ---- depthwise 3x3 kernel configurations
+// A choice is kept as a ConvKernel: fam 0 = register kernel (tile = strips
+// per work item), fam 1 = band kernel (tile = rows | strips << 8, split =
+// threads per workgroup).
+
+// Band kernel geometry for bands of rb output rows and column tiles of ct
+// strips (ct is capped at the strips of a row); false when the shape or
+// the LDS size does not allow it.  threads == 0: one thread per strip and
+// 4 channels of a tile, at most 512.
+bool dw_band_config(DwArgs &a, int rb, int ct, int threads)
+{
+    a.band = 0;
+    const int C = a.C, P = dw3_pixels();
+    if (rb < 1 || rb > 64 || ct < 1 || ((int64_t)a.W * C) % 16 != 0 || (a.sh != 1 && a.sh != 2) ||
+        (a.sw != 1 && a.sw != 2))
+        return false;
+    const int nstrip = (a.Wo + P - 1) / P;
+    ct = std::min(ct, nstrip);
+    const int nct = (nstrip + ct - 1) / ct;
+    if (nct > 1 && C % 16 != 0)
+        return false;   // column tiles start on 16-byte boundaries
+    const int lcols = (ct * P - 1) * a.sw + 3;                  // LDS columns of a tile
+    const int loff0 = nct > 1 ? 0 : (16 - (a.pl * C) % 16) % 16;  // image column 0 16-aligned
+    const int64_t rowb = (int64_t)align_up((size_t)loff0 + (size_t)lcols * C, 16) + 16;
+    const int64_t bytes = ((int64_t)(rb - 1) * a.sh + 3) * rowb;
+    if (bytes > 65536)
+        return false;
+    const int64_t items = (int64_t)(C / 4) * ct;
+    if (threads == 0)
+        threads = (int)std::min<int64_t>(512, (items + 63) / 64 * 64);
+    if (threads < 64 || threads > 512 || threads % 64 != 0)
+        return false;
+    const int nband = (a.Ho + rb - 1) / rb;
+    if ((int64_t)a.N * nband * nct >= (int64_t(1) << 31) - 8)
+        return false;
+    a.band = 1;
+    a.rb = rb;
+    a.nband = nband;
+    a.ct = ct;
+    a.nct = nct;
+    a.lcols = lcols;
+    a.loff0 = loff0;
+    a.lrs = (int32_t)rowb;
+    a.lbytes = (int32_t)bytes;
+    a.bthreads = threads;
+    return true;
+}
+
+bool dw_apply(DwArgs &a, const ConvKernel &k)
+{
+    if (k.fam == 1)
+        return dw_band_config(a, k.tile & 255, k.tile >> 8, k.split);
+    const int P = dw3_pixels(), seg = k.tile;
+    if (seg != 1 && seg != 2 && seg != 4)
+        return false;
+    const int64_t items = (int64_t)a.N * a.Ho * ((a.Wo + P * seg - 1) / (P * seg)) * (a.C / 8);
+    if (items >= (int64_t(1) << 31))
+        return false;
+    a.band = 0;
+    a.seg = seg;
+    a.items = (int32_t)items;
+    return true;
+}
+
+// Candidates: the register kernel (its default segment length first, the
+// choice when nothing is timed), then band heights of 2, 4 and 8 rows with
+// whole rows or 1/2, 1/4, 1/8 of a row per tile.
+std::vector<ConvKernel> dw_candidates(const DwArgs &a, int seg_default)
+{
+    const int f_band = env_int("QNN_DWBAND", 1), f_seg = env_int("QNN_DW3T", 0);
+    const int f_rb = env_int("QNN_DWRB", 0), f_ct = env_int("QNN_DWCT", 0), f_bt = env_int("QNN_DWBT", 0);
+    DwArgs t = a;
+    if (f_band != 0 && (f_rb > 0 || f_ct > 0 || f_bt > 0) &&
+        dw_band_config(t, f_rb > 0 ? f_rb : 4, f_ct > 0 ? f_ct : (1 << 20), f_bt))
+        return {{1, t.rb | (t.ct << 8), t.bthreads}};
+    if (f_seg == 1 || f_seg == 2 || f_seg == 4)
+        return {{0, f_seg, 1}};
+    std::vector<ConvKernel> c = {{0, seg_default, 1}};
+    if (f_band == 0)
+        return c;
+    for (int sg : {1, 2, 4})
+        if (sg != seg_default && dw_apply(t, {0, sg, 1}))
+            c.push_back({0, sg, 1});
+    const int nstrip = (a.Wo + dw3_pixels() - 1) / dw3_pixels();
+    for (int rb : {2, 4, 8})
+        for (int div : {1, 2, 4, 8}) {
+            const int ct = (nstrip + div - 1) / div;
+            if (!dw_band_config(t, rb, ct, 0))
+                continue;
+            const ConvKernel k = {1, t.rb | (t.ct << 8), t.bthreads};
+            bool dup = false;
+            for (const ConvKernel &o : c)
+                dup = dup || (o.fam == k.fam && o.tile == k.tile && o.split == k.split);
+            if (!dup)
+                c.push_back(k);
+        }
+    return c;
+}
+
+std::string dw_tune_key(const ConvDesc &d)
+{
+    bool zpw = false;
+    for (int i = 0; i < d.wq.n; ++i)
+        zpw = zpw || d.wq.zero_point[i] != 0;
+    char buf[256];
+    snprintf(buf, sizeof buf, "dw:x%d:n%d:h%d:w%d:c%d:r%d:s%d:st%dx%d:p%d,%d,%d,%d:y%d:q%d:z%d:l%d,%d", (int)d.xt,
+             d.N, d.H, d.W, d.C, d.R, d.S, d.cp.stride_h, d.cp.stride_w, d.cp.pad_top, d.cp.pad_bottom,
+             d.cp.pad_left, d.cp.pad_right, (int)d.yt, (int)d.rnd, (int)zpw, d.y_ldc, d.y_coff);
+    return buf;
+}
+
+// Times the depthwise candidates on the plan's shape (constant-filled
+// activations, cold caches as in autotune_conv) and returns the fastest.
+qnn_status autotune_dw(const DwArgs &base, const std::vector<ConvKernel> &cands, hipStream_t st, ConvKernel *best)
+{
+    const size_t xb = align_up((size_t)base.N * base.H * base.W * base.C, 256);
+    const size_t yb = align_up((size_t)base.N * base.Ho * base.Wo * base.y_ldc * (base.out_i32 ? 4 : 1), 256);
+    void *buf = nullptr;
+    hipError_t e = hipMalloc(&buf, xb + yb + 256);
+    if (e != hipSuccess)
+        return fail(QNN_ERR_ALLOC, "hipMalloc of %zu bytes for kernel tuning failed", xb + yb + 256);
+    const size_t flush_bytes = size_t(320) << 20;
+    void *flush = nullptr;
+    if (hipMalloc(&flush, flush_bytes) != hipSuccess)
+        flush = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    qnn_status s = QNN_OK;
+    float best_ms = 1e30f;
+    auto launch = [&](const DwArgs &t) { return t.band ? launch_depthwise3_band(t, st) : launch_depthwise3(t, st); };
+    if ((e = hipMemsetAsync(buf, 0x35, xb + yb + 256, st)) != hipSuccess || (e = hipEventCreate(&e0)) != hipSuccess ||
+        (e = hipEventCreate(&e1)) != hipSuccess) {
+        s = hip_fail(e, "kernel tuning set-up");
+    } else {
+        for (const ConvKernel &k : cands) {
+            DwArgs t = base;
+            t.x = (const uint8_t *)buf;
+            t.y = (char *)buf + xb;
+            if (!dw_apply(t, k))
+                continue;
+            t.vec_store = t.band ? t.y_ldc % 4 == 0 && t.y_coff % 4 == 0 : t.y_ldc % 8 == 0 && t.y_coff % 8 == 0;
+            if ((e = launch(t)) != hipSuccess)
+                break;
+            constexpr int kRuns = 5;
+            float runs[kRuns];
+            for (int r = 0; r < kRuns && e == hipSuccess; ++r) {
+                if (flush && ((e = launch_cache_sweep(flush, flush_bytes, (int *)((char *)buf + xb + yb), st)) !=
+                                  hipSuccess ||
+                              (e = hipMemsetAsync(flush, r, size_t(16) << 20, st)) != hipSuccess))
+                    break;
+                if ((e = hipEventRecord(e0, st)) != hipSuccess || (e = launch(t)) != hipSuccess ||
+                    (e = hipEventRecord(e1, st)) != hipSuccess || (e = hipEventSynchronize(e1)) != hipSuccess ||
+                    (e = hipEventElapsedTime(&runs[r], e0, e1)) != hipSuccess)
+                    break;
+            }
+            if (e != hipSuccess)
+                break;
+            std::sort(runs, runs + kRuns);
+            if (runs[kRuns / 2] < best_ms) {
+                best_ms = runs[kRuns / 2];
+                *best = k;
+            }
+        }
+        if (e != hipSuccess)
+            s = hip_fail(e, "depthwise kernel tuning");
+    }
+    if (e0)
+        (void)hipEventDestroy(e0);
+    if (e1)
+        (void)hipEventDestroy(e1);
+    (void)hipStreamSynchronize(st);
+    (void)hipFree(buf);
+    if (flush)
+        (void)hipFree(flush);
+    return s;
+}
+
 qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, bool tune = true)
 {
     int32_t Ho, Wo, lo, hi;
@@ -722,7 +898,25 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
         const int C = d.C, RS = d.R * d.S;
         // 3x3 layers run on the dot-product kernel; the general kernel's
         // weights are kept too (unaligned x, other filter sizes)
-        const int64_t dw3_items = (int64_t)d.N * Ho * ((Wo + dw3_pixels() - 1) / dw3_pixels()) * (C / 8);
+        // strips per work item: the longest segment that still leaves about
+        // 16 waves per CU (QNN_DW3T=1|2|4 forces one)
+        int seg = 1;
+        {
+            const int f = env_int("QNN_DW3T", 0);
+            if (f == 1 || f == 2 || f == 4) {
+                seg = f;
+            } else {
+                for (int t : {4, 2}) {
+                    const int64_t it = (int64_t)d.N * Ho * ((Wo + dw3_pixels() * t - 1) / (dw3_pixels() * t)) * (C / 8);
+                    if (it / 64 >= 16 * device_cus()) {
+                        seg = t;
+                        break;
+                    }
+                }
+            }
+        }
+        const int64_t dw3_items =
+            (int64_t)d.N * Ho * ((Wo + dw3_pixels() * seg - 1) / (dw3_pixels() * seg)) * (C / 8);
         const bool dw3 = d.R == 3 && d.S == 3 && d.cp.dil_h == 1 && d.cp.dil_w == 1 && C % 8 == 0 &&
                          (d.cp.stride_w == 1 || d.cp.stride_w == 2) && dw3_items < (int64_t(1) << 31) &&
                          (int64_t)d.N * d.H * d.W * C < (int64_t(1) << 31) &&
@@ -801,12 +995,44 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
         a.lo_off = lo + off8;
         a.hi_off = hi + off8;
         a.out_xor = off8 ? 0x80808080u : 0u;
+        a.seg = seg;
         a.items = dw3 ? (int32_t)dw3_items : 0;
+        // kernel choice among the register kernel's segment lengths and the
+        // band kernel's band heights and column tiles, timed on this shape
+        // (QNN_DWBAND=0 keeps the register kernel; QNN_DWRB=<rows>,
+        // QNN_DWCT=<strips>, QNN_DWBT=<threads> force a band configuration)
+        a.band = 0;
+        if (dw3) {
+            const std::vector<ConvKernel> cands = dw_candidates(a, seg);
+            ConvKernel best = cands[0];
+            if (cands.size() > 1 && M > 0 && tune && env_int("QNN_AUTOTUNE", 1) != 0) {
+                const std::string key = dw_tune_key(d);
+                if (!tune_lookup(key, cands, &best)) {
+                    DwArgs t = a;
+                    t.chan = chan3;
+                    if ((s = autotune_dw(t, cands, st, &best)) != QNN_OK) {
+                        free_plan(p);
+                        return s;
+                    }
+                    tune_record(key, best);
+                }
+            }
+            if (!dw_apply(a, best))
+                a.band = 0;
+        }
         p->dw3 = dw3;
         p->chan3 = chan3;
         char buf[128];
-        snprintf(buf, sizeof buf, "depthwise%s %dx%d stride %dx%d M=%lld C=%d", dw3 ? " dot4" : "", d.R, d.S, a.sh,
-                 a.sw, (long long)M, C);
+        if (dw3 && a.band)
+            snprintf(buf, sizeof buf,
+                     "depthwise band %dx%d stride %dx%d M=%lld C=%d rows=%d strips=%d threads=%d lds=%d", d.R, d.S,
+                     a.sh, a.sw, (long long)M, C, a.rb, a.ct, a.bthreads, a.lbytes);
+        else if (dw3)
+            snprintf(buf, sizeof buf, "depthwise dot4 %dx%d stride %dx%d M=%lld C=%d seg=%d", d.R, d.S, a.sh, a.sw,
+                     (long long)M, C, seg);
+        else
+            snprintf(buf, sizeof buf, "depthwise %dx%d stride %dx%d M=%lld C=%d", d.R, d.S, a.sh, a.sw,
+                     (long long)M, C);
         p->desc = buf;
         *out = p;
         return QNN_OK;
@@ -1170,7 +1396,11 @@ qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y
         a.x = (const uint8_t *)x;
         a.y = y;
         hipError_t e;
-        if (p->dw3 && ((uintptr_t)x & 7) == 0) {
+        if (p->dw3 && a.band && ((uintptr_t)x & 15) == 0) {
+            a.chan = p->chan3;
+            a.vec_store = ((uintptr_t)y & 3) == 0 && a.y_ldc % 4 == 0 && a.y_coff % 4 == 0;
+            e = launch_depthwise3_band(a, st);
+        } else if (p->dw3 && ((uintptr_t)x & 7) == 0) {
             a.chan = p->chan3;
             a.vec_store = ((uintptr_t)y & 7) == 0 && a.y_ldc % 8 == 0 && a.y_coff % 8 == 0;
             e = launch_depthwise3(a, st);

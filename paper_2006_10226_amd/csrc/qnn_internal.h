@@ -162,7 +162,15 @@ struct DwArgs {
     int32_t lo_off, hi_off; // clamp + off for the 32-bit path
     uint32_t out_xor;       // 0x80808080 for int8 outputs of the 32-bit path
     int32_t vec_store;      // 8-byte output stores allowed
-    int32_t items;          // work items: N * Ho * ceil(Wo / dw3_pixels()) * C / 8 (< 2^31)
+    // LDS-tiled form (band kernel): a workgroup per band of rb output rows
+    // and tile of ct strips of one image; the tile's input rows sit in LDS,
+    // row stride lrs bytes, LDS column j at byte loff0 + j * C, lcols columns
+    int32_t band;           // the band kernel may run (shape and LDS size fit)
+    int32_t rb, nband;      // output rows per band, bands per image
+    int32_t ct, nct;        // strips per column tile, column tiles per row
+    int32_t lrs, loff0, lcols, lbytes, bthreads;
+    int32_t seg;            // strips of dw3_pixels() output pixels per work item: 1, 2 or 4
+    int32_t items;          // work items: N * Ho * ceil(Wo / (dw3_pixels() * seg)) * C / 8 (< 2^31)
 };
 
 // Elementwise requantize / add arguments.
@@ -331,6 +339,7 @@ hipError_t launch_prep_dw3(const int8_t *w, const int32_t *bias, int C, int32_t 
                            uint32_t *wd, ChanRec *chan, hipStream_t st);
 hipError_t launch_depthwise3(const DwArgs &a, hipStream_t st);
 int dw3_pixels();   // output pixels along a row per work item of launch_depthwise3
+hipError_t launch_depthwise3_band(const DwArgs &a, hipStream_t st);
 hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, hipStream_t st);
 // Reads `bytes` (a multiple of 16) of `buf` through the caches (kernel
 // tuning uses it to evict what a timed launch would otherwise find cached).

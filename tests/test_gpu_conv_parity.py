@@ -429,24 +429,61 @@ DW3_SHAPES = [
     (W.ConvLayer("d", 11, 9, 16, 16, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2, dict(yt="i32", zp_w="tensor")),
     (W.ConvLayer("d", 8, 7, 64, 64, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, dict(rounding="half_away")),
     (W.ConvLayer("d", 5, 5, 24, 24, 3, 3, 1, (0, 0, 0, 0), depthwise=True), 4, dict(act=None)),
+    # rows of several 16-pixel segments with a ragged last one
+    (W.ConvLayer("d", 6, 37, 40, 40, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, {}),
+    (W.ConvLayer("d", 7, 75, 24, 24, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2, dict(x_dtype="i8", yt="i8")),
+    # band kernel shapes: column tiles with a ragged last strip, stride 2
+    # both ways, a two-column left pad with no right pad
+    (W.ConvLayer("d", 10, 38, 32, 32, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, {}),
+    (W.ConvLayer("d", 15, 33, 48, 48, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2, dict(zp_w="channel")),
+    (W.ConvLayer("d", 9, 20, 16, 16, 3, 3, 1, (0, 2, 1, 0), depthwise=True), 3, dict(x_dtype="i8")),
 ]
 
 
+# kernel forms of the 3x3 depthwise path: the register kernel with work
+# items of 1, 2 and 4 strips; the LDS-tiled band kernel with one-row bands
+# on 64-thread workgroups (several strips per thread), eight-row bands,
+# and four-row bands in column tiles of one strip; and whatever the plan's
+# timing picks
+DW3_KERNELS = [
+    ("seg1", dict(QNN_DWBAND=0, QNN_DW3T=1)),
+    ("seg2", dict(QNN_DWBAND=0, QNN_DW3T=2)),
+    ("seg4", dict(QNN_DWBAND=0, QNN_DW3T=4)),
+    ("band_r1_t64", dict(QNN_DWRB=1, QNN_DWBT=64)),
+    ("band_r8", dict(QNN_DWRB=8)),
+    ("band_r4_ct1", dict(QNN_DWRB=4, QNN_DWCT=1)),
+    ("timed", {}),
+]
+
+
+@pytest.mark.parametrize("kern", [k for k, _ in DW3_KERNELS])
 @pytest.mark.parametrize("i", range(len(DW3_SHAPES)))
-def test_depthwise3x3_dot4(i):
-    """The 3x3 depthwise dot-product kernel against the oracle, and the
-    general depthwise kernel (QNN_DW3=0) on the same case."""
+def test_depthwise3x3_dot4(i, kern):
+    """The 3x3 depthwise kernels against the oracle, and the general
+    depthwise kernel (QNN_DW3=0) on the same case.  The band kernel takes
+    rows of a multiple of 16 bytes, and column tiles narrower than a row
+    only with C % 16 == 0; on the other shapes the plan keeps the register
+    kernel."""
     layer, N, kw = DW3_SHAPES[i]
     c = W.conv_case(layer, N, seed=600 + i, **kw)
-    p, keep = make_plan(c)
-    d = p.describe()
-    p.close()
-    assert d.startswith("depthwise dot4"), d
-    log(f"dw3 shape {i}: {d}")
     ref = run_oracle(c)
-    assert_equal(run_gpu(c), ref, f"dw3 shape {i} {kw}")
-    with env(QNN_DW3=0):
-        assert_equal(run_gpu(c), ref, f"dw general shape {i} {kw}")
+    cfg = dict(DW3_KERNELS)[kern]
+    with env(**cfg):
+        p, keep = make_plan(c)
+        d = p.describe()
+        p.close()
+        band_ok = (layer.W * layer.Cin) % 16 == 0 and ("QNN_DWCT" not in cfg or layer.Cin % 16 == 0)
+        if kern.startswith("seg"):
+            assert d.startswith("depthwise dot4") and f"seg={kern[3:]}" in d, d
+        elif kern.startswith("band") and band_ok:
+            assert d.startswith("depthwise band") and f"rows={cfg['QNN_DWRB']}" in d, d
+        elif kern.startswith("band"):
+            assert d.startswith("depthwise dot4"), d
+        log(f"dw3 shape {i} {kern}: {d}")
+        assert_equal(run_gpu(c), ref, f"dw3 shape {i} {kern} {kw}")
+    if kern == "seg1":
+        with env(QNN_DW3=0):
+            assert_equal(run_gpu(c), ref, f"dw general shape {i} {kw}")
 
 
 def test_depthwise3x3_slices_and_unaligned_input():
@@ -456,27 +493,33 @@ def test_depthwise3x3_slices_and_unaligned_input():
     layer = W.ConvLayer("dslice", 10, 9, 48, 48, 3, 3, 1, (1, 1, 1, 1), depthwise=True)
     c = W.conv_case(layer, 2, seed=77)
     ref = run_oracle(c)
-    for coff in (0, 5, 16):
+    for coff, kcfg in ((0, dict(QNN_DWRB=2)), (5, dict(QNN_DWRB=2)), (16, dict(QNN_DWRB=4, QNN_DWCT=1)),
+                       (2, dict(QNN_DWRB=4, QNN_DWCT=1)), (0, dict(QNN_DWBAND=0, QNN_DW3T=1)),
+                       (5, dict(QNN_DWBAND=0, QNN_DW3T=1)), (16, dict(QNN_DWBAND=0, QNN_DW3T=4)),
+                       (5, dict(QNN_DWBAND=0, QNN_DW3T=4))):
         total = 80
-        p, keep = make_plan(c, y_ldc=total, y_coff=coff)
+        with env(**kcfg):
+            p, keep = make_plan(c, y_ldc=total, y_coff=coff)
         out = torch.full((2, 10, 9, total), 77, dtype=torch.uint8, device="cuda")
         p.run(dev(c.x), out=out)
         torch.cuda.synchronize()
         p.close()
         y = out.cpu().numpy()
-        assert_equal(y[..., coff:coff + 48], ref, f"dw3 slice {coff}")
+        assert_equal(y[..., coff:coff + 48], ref, f"dw3 slice {coff} {kcfg}")
         rest = np.ones(total, bool)
         rest[coff:coff + 48] = False
         assert (y[..., rest] == 77).all()
-    # x at an odd byte offset inside a larger buffer
-    buf = torch.zeros(c.x.size + 3, dtype=torch.uint8, device="cuda")
-    xv = buf[3:].view(c.x.shape)
-    xv.copy_(dev(c.x))
-    p, keep = make_plan(c)
-    y = p.run(xv)
-    torch.cuda.synchronize()
-    p.close()
-    assert_equal(y.cpu().numpy(), ref, "dw3 unaligned x")
+    # x at an odd byte offset inside a larger buffer (the general kernel),
+    # and 8 bytes past a 16-byte boundary (the register kernel)
+    for shift in (3, 8):
+        buf = torch.zeros(c.x.size + 16, dtype=torch.uint8, device="cuda")
+        xv = buf[shift:shift + c.x.size].view(c.x.shape)
+        xv.copy_(dev(c.x))
+        p, keep = make_plan(c)
+        y = p.run(xv)
+        torch.cuda.synchronize()
+        p.close()
+        assert_equal(y.cpu().numpy(), ref, f"dw3 x at byte offset {shift}")
 
 
 @pytest.mark.parametrize("tile", list(range(12)))
