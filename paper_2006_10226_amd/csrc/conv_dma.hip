@@ -27,6 +27,7 @@
 //     and the epilogue adds it (store_tile).
 #include "conv_common.h"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace qnn {
@@ -522,24 +523,28 @@ __global__ void __launch_bounds__(256) rowpack_weights_kernel(const int8_t *w, i
 __global__ void __launch_bounds__(256) pad_image_kernel(const uint8_t *x, int N, int H, int W, int C, int Hp, int Wp,
                                                         int C4, int pt, int pl, uint8_t zp, uint8_t *out)
 {
-    const long long pix = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (pix >= (long long)N * Hp * Wp)
+    // block (bx, by): padded pixels 256 bx .. of the rows by, by + gridDim.y,
+    // ...; the row split is uniform over the block (scalar arithmetic)
+    const int w = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (w >= Wp)
         return;
-    const int w = (int)(pix % Wp);
-    const long long t = pix / Wp;
-    const int h = (int)(t % Hp), n = (int)(t / Hp);
-    const int ih = h - pt, iw = w - pl;
-    const bool in = (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
-    const uint8_t *src = x + (((size_t)n * H + (in ? ih : 0)) * W + (in ? iw : 0)) * C;
-    uint32_t *dst = (uint32_t *)(out + pix * C4);
-    for (int c0 = 0; c0 < C4; c0 += 4) {
-        uint32_t v = 0;
-        for (int e = 0; e < 4; ++e) {
-            const int c = c0 + e;
-            const uint32_t b = (in && c < C) ? src[c] : zp;
-            v |= b << (8 * e);
+    const int iw = w - pl;
+    const bool col_in = (unsigned)iw < (unsigned)W;
+    for (int row = (int)blockIdx.y; row < N * Hp; row += (int)gridDim.y) {
+        const int n = row / Hp, h = row - n * Hp;
+        const int ih = h - pt;
+        const bool in = col_in && (unsigned)ih < (unsigned)H;
+        const uint8_t *src = x + ((size_t)(n * H + (in ? ih : 0)) * W + (in ? iw : 0)) * C;
+        uint32_t *dst = (uint32_t *)(out + ((size_t)row * Wp + w) * C4);
+        for (int c0 = 0; c0 < C4; c0 += 4) {
+            uint32_t v = 0;
+            for (int e = 0; e < 4; ++e) {
+                const int c = c0 + e;
+                const uint32_t b = (in && c < C) ? src[c] : zp;
+                v |= b << (8 * e);
+            }
+            dst[c0 >> 2] = v;
         }
-        dst[c0 >> 2] = v;
     }
 }
 
@@ -555,9 +560,13 @@ hipError_t launch_rowpack_weights(const int8_t *w, int K, int R, int S, int C, i
 hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp, int Wp, int C4, int pt, int pl,
                             uint8_t zp, uint8_t *out, hipStream_t st)
 {
-    const long long n = (long long)N * Hp * Wp;
-    hipLaunchKernelGGL(pad_image_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, x, N, H, W, C, Hp, Wp,
-                       C4, pt, pl, zp, out);
+    const long long rows = (long long)N * Hp;
+    if (rows * Wp == 0)
+        return hipSuccess;
+    if (rows >= (1LL << 31))
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((Wp + 255) / 256), (unsigned)std::min<long long>(rows, 65535));
+    hipLaunchKernelGGL(pad_image_kernel, grid, dim3(256), 0, st, x, N, H, W, C, Hp, Wp, C4, pt, pl, zp, out);
     return hipGetLastError();
 }
 
