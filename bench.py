@@ -36,9 +36,10 @@ sys.path.insert(0, ROOT)
 
 # Committed kernel choices (qnn_set_tuning_file records): the plans of these
 # workloads take them instead of timing candidates on the machine at hand,
-# so the benchmark, its profiles and the full-tensor parity test of the
-# same layers run the same kernels.
-CHOICE_FILES = {"resnet50_b32": os.path.join("workloads", "choices", "resnet50_b32.txt")}
+# so the benchmark and its profiles (and, for ResNet-50 b32, the
+# full-tensor parity test of the same layers) run the same kernels.
+CHOICE_FILES = {"resnet50_b32": os.path.join("workloads", "choices", "resnet50_b32.txt"),
+                "mobilenet_v2_b64": os.path.join("workloads", "choices", "mobilenet_v2_b64.txt")}
 
 PEAK_INT8_TOPS = 5000.0   # MI355X dense int8 MFMA, TOP/s
 PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, GB/s
@@ -477,6 +478,8 @@ def main():
     ap.add_argument("--workload", default="resnet50_b32")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-warm-clock", action="store_true",
+                    help="skip the warm per-layer timing and the clock reading (short counter runs)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times), for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters, and exit")
@@ -538,9 +541,12 @@ def main():
     log(f"step {ms:.4f} ms -> {value:.1f} TOP/s (graph={graphed})")
 
     per, how = time_launches(items, args.steps)
-    warm = time_warm(items)
-    clock = sample_clock(items, graph if graphed else None)
-    log(f"GPU clock while stepping: {clock}")
+    if args.no_warm_clock:
+        warm, clock = np.full(len(items), np.nan), None
+    else:
+        warm = time_warm(items)
+        clock = sample_clock(items, graph if graphed else None)
+        log(f"GPU clock while stepping: {clock}")
     groups = {}
     for it, t in zip(items, per):
         g = kernel_group(it)
@@ -603,7 +609,7 @@ def main():
     layer_rows = []
     for it, t, h, tw in zip(items, per, how, warm):
         row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3), "timed": h,
-               "warm_us": round(float(tw) * 1e3, 3),
+               "warm_us": None if np.isnan(tw) else round(float(tw) * 1e3, 3),
                "gmac": round(it.macs / 1e9, 4), "mbytes": round(it.bytes / 1e6, 3)}
         if it.macs:
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
@@ -653,7 +659,8 @@ def main():
                    # kernel times summed over the layers: cold (inside the step, each layer's
                    # inputs last touched a step earlier) and warm (each layer repeated back to back)
                    "layer_kernel_sum_us": {"cold": round(float(np.sum(per)) * 1e3, 2),
-                                           "warm": round(float(np.sum(warm)) * 1e3, 2)},
+                                           "warm": None if args.no_warm_clock
+                                           else round(float(np.sum(warm)) * 1e3, 2)},
                    "gpu_clock_mhz": clock},
         "roofline": roof,
         "cpu_baseline": cpu,

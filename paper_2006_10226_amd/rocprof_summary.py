@@ -85,7 +85,7 @@ def group_of(kernel_name):
         cfg = _WIN_CFGS.index((nb, ks, tcb)) if (nb, ks, tcb) in _WIN_CFGS else -1
         return f"conv_window tile={16 * tcb}x64x64 threads={nb * ks * 64} stages=2 cfg={cfg}"
     base = kernel_name.split("(")[0].split("<")[0].replace("void ", "").strip()
-    if base in ("qnn::depthwise3_kernel", "qnn::depthwise_kernel"):
+    if base in ("qnn::depthwise3_kernel", "qnn::depthwise3_band_kernel", "qnn::depthwise_kernel"):
         return "depthwise"
     if base == "qnn::add_kernel":
         return "add"
