@@ -616,6 +616,8 @@ def test_every_wave_split(split):
     (W.ConvLayer("stem3p", 20, 20, 3, 40, 3, 3, 1, (1, 2, 0, 1)), 2),
     (W.ConvLayer("c8", 17, 16, 8, 24, 3, 3, 1, (1, 1, 1, 1)), 2),
     (W.ConvLayer("c4_5x5", 15, 15, 4, 70, 5, 5, 2, (2, 2, 2, 2)), 2),
+    (W.ConvLayer("c1_5x5", 27, 27, 1, 20, 5, 5, 2, (2, 1, 2, 1)), 2),
+    (W.ConvLayer("c2", 9, 40, 2, 72, 3, 3, 1, (1, 1, 1, 1)), 3),
 ])
 def test_row_pair_mode(layer, N):
     """Small channel counts (S * C4 <= 32) through the row-pair mode of the
