@@ -110,19 +110,27 @@ CHAINS = {
 }
 
 
-def setup_chain(workload):
+def setup_chain(workload, fuse=True):
     """Plans and device tensors of a chained network: every step writes its
     own output tensor (or its channel slice of a concat), which its
-    consumers read."""
+    consumers read.  fuse: each residual add that a conv's plan can run in
+    its epilogue (paper_2006_10226_amd.fusion) runs there, and the conv's
+    own output is never written."""
     import torch
     import workloads as W
     from paper_2006_10226_amd import qnn as Q
+    from paper_2006_10226_amd.fusion import residual_fusions
 
     fn, N = CHAINS[workload]
     ch = getattr(W, fn)(N)
     t = {"x0": torch.from_numpy(ch.x0).cuda()}
+    fusions = residual_fusions(ch.graph()) if fuse else {}
+    by_conv = {c: (i, r) for i, (c, r) in fusions.items()}
+    skip = set()
     items = []
-    for st in ch.steps:
+    for idx, st in enumerate(ch.steps):
+        if idx in skip:
+            continue
         it = Item()
         if isinstance(st, W.ChainConv):
             L = st.layer
@@ -139,15 +147,32 @@ def setup_chain(workload):
                 it.plan = Q.conv2d_plan(shape, "i8", s_x, zp_x, it.w, st.s_w, st.zp_w, it.bias,
                                         L.stride, L.pads, 1, st.s_y, st.zp_y, "i8", st.act, y_ldc=total, y_coff=off)
             it.x = t[st.src]
-            if st.y_off is not None and st.dst in t:
+            it.residual = None
+            if idx in by_conv:
+                ai, rname = by_conv[idx]
+                add = ch.steps[ai]
+                s_r, zp_r = ch.q[rname]
+                try:
+                    it.plan.set_residual("i8", s_r, zp_r, add.s_o, add.zp_o, "i8", act=add.act)
+                    it.residual, skip_add = t[rname], ai
+                    it.name = f"{L.name}+{add.name}"
+                except Q.QnnError:
+                    pass   # this plan's kernel has no fused epilogue: the add runs on its own
+            if it.residual is not None:
+                it.out = t[ch.steps[skip_add].dst] = it.plan.new_output()
+                skip.add(skip_add)
+            elif st.y_off is not None and st.dst in t:
                 it.out = t[st.dst]   # another branch's slice of the same concat
             else:
                 it.out = t[st.dst] = it.plan.new_output()
             it.desc = it.plan.describe()
             Nb, Ho, Wo, K = it.plan.out_shape
             it.macs = Nb * Ho * Wo * K * L.R * L.S * (1 if L.depthwise else L.Cin)
-            it.bytes = it.x.numel() + st.w.size + Nb * Ho * Wo * K
-            it.run = (lambda it=it: it.plan.run(it.x, it.out))
+            it.bytes = it.x.numel() + st.w.size + Nb * Ho * Wo * K * (1 if it.residual is None else 2)
+            if it.residual is None:
+                it.run = (lambda it=it: it.plan.run(it.x, it.out))
+            else:
+                it.run = (lambda it=it: it.plan.run(it.x, it.out, residual=it.residual))
         elif isinstance(st, W.ChainPool):
             it.kind, it.layer, it.name, it.desc = "pool", None, st.name, "pool"
             it.x = t[st.src]
@@ -169,12 +194,12 @@ def setup_chain(workload):
     return items, N
 
 
-def setup(workload):
+def setup(workload, fuse=True):
     import torch
     from paper_2006_10226_amd import qnn as Q
 
     if workload in CHAINS:
-        return setup_chain(workload)
+        return setup_chain(workload, fuse)
     layers, batch = _layers(workload)
     items = []
     for kind, layer, c in layers:
@@ -231,6 +256,8 @@ def kernel_group(it):
         extra += f" cfg={d['cfg']}"
     if "ksplit" in d:
         extra += " ksplit"
+    if getattr(it, "residual", None) is not None:
+        extra += " +add"
     return f"{words[0]} tile={d['tile']} {extra}"
 
 
@@ -274,6 +301,12 @@ def time_steps(items, steps, warmup, use_graph):
     return start.elapsed_time(end) / steps, graph
 
 
+def _timed_plan(it):
+    """Whether a step runs through qnn_plan_run_timed (plans without a fused add)."""
+    return (getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw")
+            and getattr(it, "residual", None) is None)
+
+
 def time_launches(items, steps):
     """Per-launch kernel time over `steps` eager steps, on the stream the
     kernels run on (torch's current stream).  A layer with a plan runs through
@@ -290,10 +323,10 @@ def time_launches(items, steps):
     for s in range(steps):
         for i, it in enumerate(items):
             a, b = ev[s][i]
-            if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw"):
+            if _timed_plan(it):
                 it.plan.run_timed(it.x, it.out, getattr(it, "ws", None), a, b)
             else:
-                Q.time_next_kernel(a, b)   # the add's or pool's own kernel records them
+                Q.time_next_kernel(a, b)   # the kernel itself records them (add, pool, fused conv + add)
                 it.run()
     torch.cuda.synchronize()
     per = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])  # ms
@@ -313,7 +346,7 @@ def time_warm(items, reps=10):
         it.run()
         it.run()
         for a, b in ev:
-            if getattr(it, "plan", None) is not None and it.kind in ("conv", "dense", "dw"):
+            if _timed_plan(it):
                 it.plan.run_timed(it.x, it.out, getattr(it, "ws", None), a, b)
             else:
                 Q.time_next_kernel(a, b)
@@ -477,6 +510,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="resnet50_b32")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="chained workloads: run every residual add as its own kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-warm-clock", action="store_true",
                     help="skip the warm per-layer timing and the clock reading (short counter runs)")
@@ -523,7 +558,7 @@ def main():
         from paper_2006_10226_amd import qnn
         qnn.set_tuning_file(args.tuning_file)
     log(f"setting up {args.workload}")
-    items, batch = setup(args.workload)
+    items, batch = setup(args.workload, fuse=not args.no_fuse)
     total_macs = sum(it.macs for it in items)
     total_bytes = sum(it.bytes for it in items)
     log(f"{len(items)} layers, {total_macs / 1e9:.2f} G MAC per step")
@@ -661,7 +696,10 @@ def main():
                    "layer_kernel_sum_us": {"cold": round(float(np.sum(per)) * 1e3, 2),
                                            "warm": None if args.no_warm_clock
                                            else round(float(np.sum(warm)) * 1e3, 2)},
-                   "gpu_clock_mhz": clock},
+                   "gpu_clock_mhz": clock,
+                   # residual adds run inside the epilogue of a conv (chained workloads)
+                   **({"fused_adds": sum(1 for it in items if getattr(it, "residual", None) is not None)}
+                      if args.workload in CHAINS else {})},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -374,6 +374,42 @@ qnn_status qnn_plan_run_timed(const qnn_plan *plan, void *stream, const void *x,
 qnn_status qnn_time_next_kernel(void *start_event, void *stop_event);
 
 /*
+ * Residual add fused into a conv or dense plan's epilogue.  The paper
+ * lowers QNN operators to sequences of simpler ones and relies on operator
+ * fusion to run them together (Sec. III-A, III-B); here the qnn.add that
+ * follows a conv in a residual block (qnn_add above) runs inside the conv
+ * kernel instead of as a pass of its own.  After the call the plan stores
+ *   y = qnn_add(c, r)
+ * where c is the conv output exactly as the plan computed it (y_dtype,
+ * y_q, act, rounding of the plan: the intermediate, never written) and r
+ * is a residual of r_dtype (UINT8 / INT8) with per-tensor r_q, element
+ * (pixel m, channel k) at r[m * r_ldc + r_coff + k]; the sum has o_dtype
+ * (UINT8 / INT8), o_q (per tensor), clamp `act` and `rounding` (those of
+ * qnn_add), and is stored where the plan stores its output (y_ldc,
+ * y_coff).  The bytes equal those of qnn_plan_run followed by qnn_add.
+ * Only plans whose kernel has the fused epilogue (8-bit output staged
+ * through LDS by the tap-walk or LDS-direct kernels, qnn_plan_describe
+ * starting with "conv_tap" or "conv_dma", with waves of at most 64 x 64
+ * outputs and no split reduction) and whose y_ldc and y_coff are
+ * multiples of 16 accept it;
+ * others, int32 outputs and a second call return QNN_ERR_UNSUPPORTED and
+ * leave the plan as it was.  r_ldc >= r_coff + K.  A fused plan runs only
+ * through qnn_plan_run_residual.
+ */
+qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams r_q, int32_t r_ldc,
+                                 int32_t r_coff, qnn_dtype o_dtype, qnn_qparams o_q, qnn_clamp act,
+                                 qnn_rounding rounding);
+
+/*
+ * Runs a plan with a fused residual add: as qnn_plan_run, with the
+ * residual device buffer (layout set by qnn_plan_set_residual, not
+ * overlapping y).  y must be 16-byte aligned (QNN_ERR_UNSUPPORTED, nothing
+ * enqueued).  Enqueued on `stream`, no synchronization.
+ */
+qnn_status qnn_plan_run_residual(const qnn_plan *plan, void *stream, const void *x, const void *residual, void *y,
+                                 void *workspace);
+
+/*
  * Allocation-free run, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): runs the plan like qnn_plan_run, with its workspace taken from

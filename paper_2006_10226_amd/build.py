@@ -10,7 +10,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libqnn.so")
-SOURCES = ["qnn_api.cpp", "conv_mfma.hip", "conv_tap.hip", "conv_dma.hip", "conv_wave.hip", "conv_halo.hip", "conv_window.hip", "elementwise.hip",
+SOURCES = ["qnn_api.cpp", "conv_mfma.hip", "conv_tap.hip", "conv_dma.hip", "conv_dma_fused.hip", "conv_wave.hip", "conv_halo.hip", "conv_window.hip", "elementwise.hip",
            "depthwise.hip", "pool.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -63,6 +63,77 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
     return packed;
 }
 
+// Residual qnn.add fused into the epilogue: 16 requantized output bytes
+// (channels k0 .. k0 + n - 1 of pixel m, n <= 16; dtype ydt) and the
+// residual bytes of the same elements go through add_one; the add's bytes
+// replace the outputs (those past n are not stored).
+__device__ __forceinline__ v4i residual_add16(const ConvArgs &a, v4i v, int m, int k0, int n)
+{
+    const uint8_t *rp = a.res + (size_t)m * a.r_ldc + a.r_coff + k0;
+    uint32_t r[4] = {0u, 0u, 0u, 0u};
+    if (a.res_vec && n == 16) {
+        const v4i t = __builtin_nontemporal_load((const v4i *)rp);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            r[e] = (uint32_t)t[e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+            if (e < n)
+                r[e >> 2] |= (uint32_t)rp[e] << (8 * (e & 3));
+    }
+    // one 4-byte word per pass, the words rotated through position 0 (a
+    // rolled loop keeps a single copy of add_one's code)
+    v4i o = v4i{0, 0, 0, 0};
+#pragma unroll 1
+    for (int q = 0; q < 4; ++q) {
+        uint32_t ow = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t xb = ((uint32_t)v[0] >> (8 * e)) & 0xffu;
+            const uint32_t rb = (r[0] >> (8 * e)) & 0xffu;
+            const int x = a.ydt == 1 ? (int)(int8_t)xb : (int)xb;
+            const int y = a.rdt == 1 ? (int)(int8_t)rb : (int)rb;
+            ow |= ((uint32_t)add_one(a.fadd, x, y) & 0xffu) << (8 * e);
+        }
+        o = v4i{o[1], o[2], o[3], (int)ow};
+        v = v4i{v[1], v[2], v[3], v[0]};
+        const uint32_t r0 = r[0];
+        r[0] = r[1];
+        r[1] = r[2];
+        r[2] = r[3];
+        r[3] = r0;
+    }
+    return o;
+}
+
+// Copy-out of a staged tile (TP pixel rows of SP bytes in LDS, the tile's
+// first min(TC, kmax) channels valid) with the residual add applied (a
+// rolled loop: the add's code is long and runs once per tile).
+template <int TC, int TP, int NT, int SP>
+__device__ __forceinline__ void copy_out_residual(const ConvArgs &a, const int8_t *stage, int c0, int p0, int kmax)
+{
+    constexpr int CH = TC / 16;
+#pragma unroll 1
+    for (int idx = threadIdx.x; idx < TP * CH; idx += NT) {
+        const int pl = idx / CH, qc = idx % CH;
+        const int m = p0 + pl;
+        if (m < a.M && qc * 16 < kmax) {
+            const int n = min(16, kmax - qc * 16);
+            const v4i v = residual_add16(a, *(const v4i *)(stage + pl * SP + qc * 16), m, c0 + qc * 16, n);
+            uint8_t *dst = (uint8_t *)a.y + (size_t)m * a.y_ldc + a.y_coff + c0 + qc * 16;
+            if (n == 16) {
+                __builtin_nontemporal_store(v, (v4i *)dst);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    if (e < n)
+                        dst[e] = (uint8_t)((uint32_t)v[e >> 2] >> (8 * (e & 3)));
+            }
+        }
+    }
+}
+
 // 16-byte LDS read issued as inline assembly.  The compiler orders every LDS
 // read it sees after all LDS-direct loads still in flight (it cannot tell
 // which LDS bytes they write), which drains a ring of staged K-steps at
@@ -145,14 +216,16 @@ __device__ __forceinline__ void add_bconst(v4i (&acc)[TC / WC / 16][TP / WP / 16
 // read of `stage` before the call.  `recs`, when given, holds the tile's
 // channel records (channels c0 .. c0 + TC - 1) in LDS, else they are read
 // from a.chan; with `recs` the accumulators already hold bconst (see
-// add_bconst).
-template <int TC, int TP, int WC, int WP, int STAGE_BYTES>
+// add_bconst).  FUSE: the staged copy-out applies the residual add (the
+// host launches these instantiations only with a.res set and a.staged).
+template <int TC, int TP, int WC, int WP, int STAGE_BYTES, bool FUSE = false>
 __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC / 16][TP / WP / 16], int8_t *stage,
                                            int c0, int p0, const ChanRec *recs = nullptr)
 {
     constexpr int NT = WC * WP * 64;
     constexpr int WTC = TC / WC, WTP = TP / WP;
     constexpr int FC = WTC / 16, FP = WTP / 16;
+    static_assert(!FUSE || WTC * WTP <= kFuseMaxWaveTile, "fused add: wave tiles of at most kFuseMaxWaveTile");
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
@@ -212,6 +285,10 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
         __syncthreads();
         constexpr int CH = TC / 16;
         const int kmax = a.K - c0;
+        if constexpr (FUSE) {
+            copy_out_residual<TC, TP, NT, SP>(a, stage, c0, p0, kmax);
+            return;
+        }
 #pragma unroll
         for (int it = 0; it < (TP * CH + NT - 1) / NT; ++it) {
             const int idx = it * NT + tid;

@@ -43,7 +43,8 @@ constexpr int tap_occupancy()
     return WTC * WTP >= 128 * 64 ? 1 : 2;
 }
 
-template <int TC, int TP, int BK, int WC, int WP>
+// FUSE: the epilogue applies the residual add (store_tile).
+template <int TC, int TP, int BK, int WC, int WP, bool FUSE = false>
 __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>())) conv_tap_kernel(ConvArgs a)
 {
     constexpr int NT = WC * WP * 64;
@@ -249,7 +250,7 @@ __global__ void __launch_bounds__(WC *WP * 64, (tap_occupancy<TC / WC, TP / WP>(
     // the record loads (LDS-direct) have landed before anyone reads them
     __builtin_amdgcn_s_waitcnt((0) | (7 << 4) | (15 << 8) | (0 << 14));
     __syncthreads();
-    store_tile<TC, TP, WC, WP, 2 * STAGE>(a, acc, lds, c0, p0, recs);
+    store_tile<TC, TP, WC, WP, 2 * STAGE, FUSE>(a, acc, lds, c0, p0, recs);
 }
 
 // TapTile -> tile, K-step and wave grid.
@@ -268,6 +269,11 @@ TileShape tap_tile_shape(int tile)
     return {c.tc, c.tp, c.bk};
 }
 
+int tap_wave_tile(int tile)
+{
+    return kTapCfg[tile].tc / kTapCfg[tile].wc * (kTapCfg[tile].tp / kTapCfg[tile].wp);
+}
+
 int tap_threads(int tile)
 {
     return kTapCfg[tile].wc * kTapCfg[tile].wp * 64;
@@ -278,8 +284,16 @@ static hipError_t launch_tap_cfg(const ConvArgs &a, hipStream_t st)
 {
     constexpr TapCfg c = kTapCfg[T];
     const int grid = (a.ntiles + 7) / 8 * 8;
-    launch_main((conv_tap_kernel<c.tc, c.tp, c.bk, c.wc, c.wp>), dim3(grid), dim3(c.wc * c.wp * 64), 0, st,
-                       a);
+    if (a.res) {
+        if constexpr (c.tc / c.wc * (c.tp / c.wp) <= kFuseMaxWaveTile)
+            launch_main((conv_tap_kernel<c.tc, c.tp, c.bk, c.wc, c.wp, true>), dim3(grid), dim3(c.wc * c.wp * 64),
+                        0, st, a);
+        else
+            return hipErrorInvalidValue;   // no fused-add instantiation
+    } else {
+        launch_main((conv_tap_kernel<c.tc, c.tp, c.bk, c.wc, c.wp>), dim3(grid), dim3(c.wc * c.wp * 64), 0, st,
+                    a);
+    }
     return hipGetLastError();
 }
 

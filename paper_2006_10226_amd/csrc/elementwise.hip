@@ -17,11 +17,6 @@ namespace qnn {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int clampll(long long v, int lo, int hi)
-{
-    return (int)(v < lo ? lo : (v > hi ? hi : v));
-}
-
 // ------------------------------------------------------------- depthwise
 
 template <bool VEC4, bool OUT_I32>
@@ -217,29 +212,6 @@ __global__ void __launch_bounds__(256) requantize_kernel(ReqArgs a)
             }
         }
     }
-}
-
-// round(v * mult / 2^shift), ties up, for |v| < 2^9 and shift = np + 16 with
-// np in [1, 24], from full-rate 24-bit multiplies: p = v * mult = p1 * 2^16 +
-// p0 with p1 = v * mh and p0 = v * ml (both exact in 32 bits), so that
-// p + 2^(shift-1) = (p1 + c + floor(p0 / 2^16)) * 2^16 + (p0 mod 2^16), and
-// the remainder below 2^16 cannot change the floor of the division by
-// 2^shift.
-__device__ __forceinline__ int round_mul_shift_small(int v, int mh, int ml, int np, int c)
-{
-    return (__mul24(v, mh) + c + (__mul24(v, ml) >> 16)) >> np;
-}
-
-__device__ __forceinline__ int add_one(const AddArgs &a, int x, int y)
-{
-    if (a.fast) {
-        const int t = round_mul_shift_small(x - a.zpa, a.mah, a.mal, a.npa, a.ca) +
-                      round_mul_shift_small(y - a.zpb, a.mbh, a.mbl, a.npb, a.cb);
-        return clamp_i32(t + a.zp_y, a.lo, a.hi);
-    }
-    const long long t = rounding_mul_shift<true>(x - a.zpa, a.ma, a.na, a.rounding) +
-                        rounding_mul_shift<true>(y - a.zpb, a.mb, a.nb, a.rounding);
-    return clampll(t + a.zp_y, a.lo, a.hi);
 }
 
 template <int ADT, int BDT, int YDT, bool VEC>

@@ -160,6 +160,12 @@ struct qnn_plan {
     int avec = 16, mode = OUT_REQUANT;
     ConvKernel ker;             // kernel family and tile that run_plan launches
     bool term3 = false;
+    // the conv output's own quantization (the first input of a fused
+    // residual add), and whether an add is fused (qnn_plan_set_residual)
+    float y_scale = 1.0f;
+    int32_t y_zp = 0;
+    int y_dt = QNN_UINT8;
+    bool fused = false;
     size_t ws_asum_bytes = 0, ws_xpad_bytes = 0;
     size_t ws_cnt_bytes = 0, ws_part_bytes = 0;   // split reduction: counters, partial sums
     int32_t C_in = 0;           // channels of the caller's x (before padding to a.C)
@@ -1189,6 +1195,9 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
     a.K = d.K; a.Kpad = Kpad; a.J = (int)Jg; a.Jpad = Jpad; a.M = (int)M;
     p->C_in = d.C;
     p->pad_zp = (uint8_t)zpx;
+    p->y_scale = d.yt == QNN_INT32 ? 1.0f : d.yq.scale[0];
+    p->y_zp = d.yt == QNN_INT32 ? 0 : d.yq.zero_point[0];
+    p->y_dt = d.yt;
     a.flip4 = d.xt == QNN_UINT8 ? 0x80808080u : 0u;
     a.ydt = d.yt;
     a.lo = lo; a.hi = hi;
@@ -1335,8 +1344,13 @@ qnn_status make_conv_plan(const ConvDesc &d, hipStream_t st, qnn_plan **out, boo
 // reduction's arrival counters (zero between runs), `ws` the window sums,
 // the padded input copy and the partial sums, in that order.  A workspace
 // of qnn_plan_workspace_size bytes holds the counters first, then the rest.
-qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *cnt, void *ws)
+qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *cnt, void *ws,
+                       const void *res = nullptr)
 {
+    if (p->fused != (res != nullptr))
+        return fail(p->fused ? QNN_ERR_NULL : QNN_ERR_UNSUPPORTED,
+                    p->fused ? "plan_run: the plan adds a residual; run it with qnn_plan_run_residual and a residual"
+                             : "plan_run: a residual was given to a plan without a fused add");
     switch (p->kind) {
     case PLAN_CONV: {
         ConvArgs a = p->conv;
@@ -1346,6 +1360,10 @@ qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y
             return fail(QNN_ERR_NULL, "plan_run: x or y is NULL");
         a.x = (const uint8_t *)x;
         a.y = y;
+        if (res) {
+            a.res = (const uint8_t *)res;
+            a.res_vec = ((uintptr_t)res & 15) == 0 && a.r_ldc % 16 == 0 && a.r_coff % 16 == 0;
+        }
         if (p->ws_bytes) {
             if (!ws || (p->ws_cnt_bytes && !cnt))
                 return fail(QNN_ERR_NULL, "plan_run: the plan needs a workspace");
@@ -1381,6 +1399,8 @@ qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y
         // whole-row 16-byte stores need a 16-byte aligned row start for every pixel
         if (a.staged && (((uintptr_t)y & 15) != 0 || a.y_ldc % 16 != 0 || a.y_coff % 16 != 0))
             a.staged = 0;
+        if (a.res && !a.staged)
+            return fail(QNN_ERR_UNSUPPORTED, "plan_run_residual: y must be 16-byte aligned for the fused add");
         if (p->term3 && (e = launch_window_sums(a, (int32_t *)a.asum, st)) != hipSuccess)
             return hip_fail(e, "window-sum launch");
         if ((e = launch_conv_kernel(a, p->ker, p->avec, st)) != hipSuccess)
@@ -1425,12 +1445,12 @@ qnn_status run_plan_at(const qnn_plan *p, hipStream_t st, const void *x, void *y
     return fail(QNN_ERR_UNSUPPORTED, "unknown plan kind");
 }
 
-qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *ws)
+qnn_status run_plan(const qnn_plan *p, hipStream_t st, const void *x, void *y, void *ws, const void *res = nullptr)
 {
     if (!ws)
         ws = p->ws_own;
     char *base = (char *)ws;
-    return run_plan_at(p, st, x, y, base, base ? base + p->ws_cnt_bytes : nullptr);
+    return run_plan_at(p, st, x, y, base, base ? base + p->ws_cnt_bytes : nullptr, res);
 }
 
 qnn_status alloc_ws(qnn_plan *p)
@@ -1822,9 +1842,10 @@ qnn_status qnn_pool2d(void *stream, const void *x, qnn_dtype dtype, int32_t N, i
     return e == hipSuccess ? QNN_OK : hip_fail(e, "pool2d launch");
 }
 
-qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a_q, const void *b,
-                   qnn_dtype b_dtype, qnn_qparams b_q, int64_t count, void *y, qnn_dtype y_dtype,
-                   qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding)
+// qnn.add parameters: each operand requantized to the output scale,
+// summed, zp_y added, clamped to the output dtype and activation.
+qnn_status make_add_args(qnn_dtype a_dtype, qnn_qparams a_q, qnn_dtype b_dtype, qnn_qparams b_q, qnn_dtype y_dtype,
+                         qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding, AddArgs *out)
 {
     if (a_dtype != QNN_UINT8 && a_dtype != QNN_INT8)
         return fail(QNN_ERR_DTYPE, "add: a must be uint8 or int8");
@@ -1834,8 +1855,6 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
         return fail(QNN_ERR_DTYPE, "add: y must be uint8 or int8");
     if (rounding < QNN_ROUND_HALF_UP || rounding > QNN_ROUND_TWO_STAGE)
         return fail(QNN_ERR_QPARAM, "add: unknown rounding %d", (int)rounding);
-    if (count < 0)
-        return fail(QNN_ERR_SHAPE, "add: count must be >= 0");
     qnn_status s;
     if ((s = check_qparams(a_q, "a qparams", 1, a_dtype, false)) != QNN_OK ||
         (s = check_qparams(b_q, "b qparams", 1, b_dtype, false)) != QNN_OK ||
@@ -1850,14 +1869,6 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
         return fail(QNN_ERR_QPARAM, "add: multiplier out of range (%g, %g)", Ma, Mb);
     args.na = std::min(args.na, 63);
     args.nb = std::min(args.nb, 63);
-    if (count == 0)
-        return QNN_OK;
-    if (!a || !b || !y)
-        return fail(QNN_ERR_NULL, "add: a, b or y is NULL");
-    args.a = a;
-    args.b = b;
-    args.y = y;
-    args.count = count;
     args.zpa = a_q.zero_point[0];
     args.zpb = b_q.zero_point[0];
     args.zp_y = y_q.zero_point[0];
@@ -1876,9 +1887,87 @@ qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a
         args.npb = args.nb - 16;
         args.cb = 1 << (args.npb - 1);
     }
+    *out = args;
+    return QNN_OK;
+}
+
+qnn_status qnn_add(void *stream, const void *a, qnn_dtype a_dtype, qnn_qparams a_q, const void *b,
+                   qnn_dtype b_dtype, qnn_qparams b_q, int64_t count, void *y, qnn_dtype y_dtype,
+                   qnn_qparams y_q, qnn_clamp act, qnn_rounding rounding)
+{
+    AddArgs args{};
+    qnn_status s = make_add_args(a_dtype, a_q, b_dtype, b_q, y_dtype, y_q, act, rounding, &args);
+    if (s != QNN_OK)
+        return s;
+    if (count < 0)
+        return fail(QNN_ERR_SHAPE, "add: count must be >= 0");
+    if (count == 0)
+        return QNN_OK;
+    if (!a || !b || !y)
+        return fail(QNN_ERR_NULL, "add: a, b or y is NULL");
+    args.a = a;
+    args.b = b;
+    args.y = y;
+    args.count = count;
     const bool aligned = (((uintptr_t)a | (uintptr_t)b | (uintptr_t)y) & 15) == 0;
     const hipError_t e = launch_add(args, a_dtype, b_dtype, y_dtype, aligned, (hipStream_t)stream);
     return e == hipSuccess ? QNN_OK : hip_fail(e, "add launch");
+}
+
+qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams r_q, int32_t r_ldc, int32_t r_coff,
+                                 qnn_dtype o_dtype, qnn_qparams o_q, qnn_clamp act, qnn_rounding rounding)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_set_residual: plan is NULL");
+    if (plan->kind != PLAN_CONV)
+        return fail(QNN_ERR_UNSUPPORTED, "plan_set_residual: conv and dense plans only");
+    if (plan->fused)
+        return fail(QNN_ERR_UNSUPPORTED, "plan_set_residual: the plan already adds a residual");
+    const ConvArgs &c = plan->conv;
+    const int wave_tile = plan->ker.fam == FAM_DMA   ? dma_wave_tile(plan->ker.tile)
+                          : plan->ker.fam == FAM_TAP ? tap_wave_tile(plan->ker.tile)
+                                                     : 0;
+    if (plan->mode != OUT_REQUANT || !c.staged || wave_tile == 0 || wave_tile > kFuseMaxWaveTile)
+        return fail(QNN_ERR_UNSUPPORTED,
+                    "plan_set_residual: the plan's kernel has no fused-add epilogue (8-bit output staged by the "
+                    "tap-walk or LDS-direct kernels whose waves hold at most 64 x 64 outputs)");
+    if (c.ksplit > 1)
+        return fail(QNN_ERR_UNSUPPORTED, "plan_set_residual: the plan's kernel splits the reduction (the fused add "
+                                         "has no split form)");
+    if (c.y_ldc % 16 != 0 || c.y_coff % 16 != 0)
+        return fail(QNN_ERR_UNSUPPORTED, "plan_set_residual: the fused add stores 16-byte output rows; y_ldc %d and "
+                                         "y_coff %d must be multiples of 16", c.y_ldc, c.y_coff);
+    if (r_coff < 0 || r_ldc < (int64_t)r_coff + c.K)
+        return fail(QNN_ERR_SHAPE, "plan_set_residual: residual row stride %d and channel offset %d do not hold %d "
+                                   "channels", r_ldc, r_coff, c.K);
+    if ((int64_t)c.M * r_ldc >= (int64_t(1) << 31))
+        return fail(QNN_ERR_UNSUPPORTED, "plan_set_residual: residual of 2^31 bytes or more");
+    const float ys = plan->y_scale;
+    const int32_t yz = plan->y_zp;
+    const qnn_qparams y_q{&ys, &yz, 1};
+    AddArgs args{};
+    qnn_status s = make_add_args((qnn_dtype)plan->y_dt, y_q, r_dtype, r_q, o_dtype, o_q, act, rounding, &args);
+    if (s != QNN_OK)
+        return s;
+    plan->conv.fadd = args;
+    plan->conv.r_ldc = r_ldc;
+    plan->conv.r_coff = r_coff;
+    plan->conv.rdt = r_dtype == QNN_INT8 ? 1 : 0;
+    plan->fused = true;
+    plan->desc += " +add";
+    return QNN_OK;
+}
+
+qnn_status qnn_plan_run_residual(const qnn_plan *plan, void *stream, const void *x, const void *residual, void *y,
+                                 void *workspace)
+{
+    if (!plan)
+        return fail(QNN_ERR_NULL, "plan_run_residual: plan is NULL");
+    if (!plan->fused)
+        return fail(QNN_ERR_UNSUPPORTED, "plan_run_residual: the plan adds no residual (qnn_plan_set_residual)");
+    if (!residual)
+        return fail(QNN_ERR_NULL, "plan_run_residual: residual is NULL");
+    return run_plan(plan, (hipStream_t)stream, x, y, workspace, residual);
 }
 
 qnn_status qnn_conv2d_plan_create(qnn_plan **plan, void *stream, qnn_dtype x_dtype, int32_t N, int32_t H,

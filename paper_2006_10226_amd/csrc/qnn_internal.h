@@ -92,6 +92,59 @@ __device__ __forceinline__ int clamp_i32(int t, int lo, int hi)
     return r;
 }
 
+__device__ __forceinline__ int clampll(long long v, int lo, int hi)
+{
+    return (int)(v < lo ? lo : (v > hi ? hi : v));
+}
+
+// qnn.add arguments (the standalone add kernel, and the residual add fused
+// into a conv epilogue).
+struct AddArgs {
+    const void *a;
+    const void *b;
+    void *y;
+    int64_t count;
+    int32_t ma, na, zpa, mb, nb, zpb, zp_y;
+    int32_t lo, hi, rounding;
+    // HALF_UP with both shifts in [17, 40]: each operand's rounding from two
+    // 24-bit products (multiplier halves mh = mult >> 16, ml = mult & 0xffff,
+    // np = shift - 16, c = 2^(np - 1)); the operands are 8-bit, so the
+    // zero-point-adjusted values fit 9 bits
+    int32_t fast, mah, mal, npa, ca, mbh, mbl, npb, cb;
+};
+
+// round(v * mult / 2^shift), ties up, for |v| < 2^9 and shift = np + 16 with
+// np in [1, 24], from full-rate 24-bit multiplies: p = v * mult = p1 * 2^16 +
+// p0 with p1 = v * mh and p0 = v * ml (both exact in 32 bits), so that
+// p + 2^(shift-1) = (p1 + c + floor(p0 / 2^16)) * 2^16 + (p0 mod 2^16), and
+// the remainder below 2^16 cannot change the floor of the division by
+// 2^shift.
+__device__ __forceinline__ int round_mul_shift_small(int v, int mh, int ml, int np, int c)
+{
+    return (__mul24(v, mh) + c + (__mul24(v, ml) >> 16)) >> np;
+}
+
+// One element of qnn.add: each operand requantized to the output scale
+// (x - zp_a) * Ma, (y - zp_b) * Mb, summed, zp_y added, clamped.
+__device__ __forceinline__ int add_one(const AddArgs &a, int x, int y)
+{
+    if (a.fast) {
+        const int t = round_mul_shift_small(x - a.zpa, a.mah, a.mal, a.npa, a.ca) +
+                      round_mul_shift_small(y - a.zpb, a.mbh, a.mbl, a.npb, a.cb);
+        return clamp_i32(t + a.zp_y, a.lo, a.hi);
+    }
+    const long long t = rounding_mul_shift<true>(x - a.zpa, a.ma, a.na, a.rounding) +
+                        rounding_mul_shift<true>(y - a.zpb, a.mb, a.nb, a.rounding);
+    return clampll(t + a.zp_y, a.lo, a.hi);
+}
+
+// Largest wave tile (channels x pixels of one wave) whose epilogue holds
+// the fused residual add: waves with larger tiles keep their accumulators
+// in most of the register file, and the extra code would spill to
+// scratch, whose memory operations share the vector-memory counter that
+// the stage waits of the LDS-direct kernels count.
+constexpr int kFuseMaxWaveTile = 64 * 64;
+
 // Implicit-GEMM conv arguments.  GEMM view: D[k][m] = sum_j Wp[k][j] * X'[m][j]
 // with m = output pixel, k = output channel, j = (r*S + s)*C + c.
 struct ConvArgs {
@@ -137,6 +190,14 @@ struct ConvArgs {
     int32_t ksplit;
     int32_t *part;
     int32_t *cnt;
+    // residual qnn.add fused into the epilogue (staged 8-bit outputs of the
+    // kernels that use store_tile): the requantized conv output of channel
+    // k at pixel m (dtype ydt) and the residual res[m * r_ldc + r_coff + k]
+    // (rdt: 0 uint8, 1 int8) go through add_one(fadd, ., .); the result is
+    // stored in place of the conv output.  res == nullptr: no add.
+    const uint8_t *res;
+    int32_t r_ldc, r_coff, rdt, res_vec;   // res_vec: 16-byte residual rows are 16-byte aligned
+    AddArgs fadd;
 };
 
 // Depthwise conv arguments (channel multiplier 1).
@@ -184,19 +245,6 @@ struct ReqArgs {
     int32_t lo, hi, rounding;
 };
 
-struct AddArgs {
-    const void *a;
-    const void *b;
-    void *y;
-    int64_t count;
-    int32_t ma, na, zpa, mb, nb, zpb, zp_y;
-    int32_t lo, hi, rounding;
-    // HALF_UP with both shifts in [17, 40]: each operand's rounding from two
-    // 24-bit products (multiplier halves mh = mult >> 16, ml = mult & 0xffff,
-    // np = shift - 16, c = 2^(np - 1)); the operands are 8-bit, so the
-    // zero-point-adjusted values fit 9 bits
-    int32_t fast, mah, mal, npa, ca, mbh, mbl, npb, cb;
-};
 
 // Tile configurations of the MFMA conv kernel.
 enum ConvTile {
@@ -277,6 +325,7 @@ int dma_threads(int tile);
 bool dma_splits(int tile);   // the configuration has a split-reduction form
 int dma_split(int tile);    // K-step groups sharing a tile (1 or 2)
 int dma_stages(int tile);
+int dma_wave_tile(int tile);   // channels x pixels of one wave
 bool dma_short(int tile);   // short-reduction form: at most dma_stages(tile) K-steps
 hipError_t launch_conv_dma(const ConvArgs &a, int tile, hipStream_t st);
 // Wave-independent kernel (conv_wave.hip): 64 x 64 tile per wave, split =
@@ -316,6 +365,7 @@ hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp
 hipError_t launch_border_corr(const int8_t *wp, int Kpad, int Jpad, int C4, int S, int RS, const uint32_t *rmask,
                               const uint32_t *cmask, int ncls, int32_t zpx, int32_t *corr, hipStream_t st);
 int tap_threads(int tile);
+int tap_wave_tile(int tile);   // channels x pixels of one wave
 hipError_t launch_conv_tap(const ConvArgs &a, int tile, hipStream_t st);
 
 // Activation gather width in bytes: 16 when C % 16 == 0, 8 when C % 8 == 0,

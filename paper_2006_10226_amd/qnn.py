@@ -40,7 +40,8 @@ EXPORTS = [
     "qnn_pool2d",
     "qnn_conv2d_plan_create", "qnn_depthwise_conv2d_plan_create", "qnn_dense_plan_create",
     "qnn_conv2d_plan_create_wt", "qnn_depthwise_conv2d_plan_create_wt", "qnn_dense_plan_create_wt",
-    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_timed", "qnn_time_next_kernel", "qnn_plan_run_noalloc", "qnn_plan_workspace_size",
+    "qnn_requantize_plan_create", "qnn_plan_run", "qnn_plan_run_timed", "qnn_time_next_kernel", "qnn_plan_run_noalloc",
+    "qnn_plan_set_residual", "qnn_plan_run_residual", "qnn_plan_workspace_size",
     "qnn_plan_describe", "qnn_set_tuning_file", "qnn_plan_destroy",
 ]
 
@@ -130,6 +131,10 @@ def lib() -> ctypes.CDLL:
     L.qnn_time_next_kernel.restype = st
     L.qnn_plan_run_noalloc.argtypes = [P, P, P, P]
     L.qnn_plan_run_noalloc.restype = st
+    L.qnn_plan_set_residual.argtypes = [P, st, QParams, i32, i32, st, QParams, Clamp, st]
+    L.qnn_plan_set_residual.restype = st
+    L.qnn_plan_run_residual.argtypes = [P, P, P, P, P, P]
+    L.qnn_plan_run_residual.restype = st
     L.qnn_plan_workspace_size.argtypes = [P]
     L.qnn_plan_workspace_size.restype = ctypes.c_size_t
     L.qnn_plan_describe.argtypes = [P]
@@ -270,13 +275,30 @@ class Plan:
     def describe(self) -> str:
         return lib().qnn_plan_describe(self._h).decode()
 
+    def set_residual(self, r_dtype, r_scale, r_zp, o_scale, o_zp, o_dtype="u8", act=None, rounding="half_up",
+                     r_ldc=None, r_coff=0):
+        """qnn_plan_set_residual: the plan then stores qnn.add(its conv
+        output, a residual of the output's pixels) with the output qparams
+        o_*; run it with run(x, out, workspace, residual=r), r of shape
+        (N, Ho, Wo, r_ldc) (r_ldc defaults to the output channels)."""
+        N, Ho, Wo, K = self.out_shape
+        r_ldc = K if r_ldc is None else r_ldc
+        rdt, odt = _NAME_DT[r_dtype], _NAME_DT[o_dtype]
+        rq, oq = _Q(r_scale, r_zp, 1), _Q(o_scale, o_zp, 1)
+        _check(lib().qnn_plan_set_residual(self._h, rdt, rq.q, r_ldc, r_coff, odt, oq.q, _clamp(act),
+                                           _ROUND[rounding]))
+        self.out_dtype = _DT_TORCH[odt]
+        self.residual = ((N, Ho, Wo, r_ldc), _DT_TORCH[rdt])
+        return self
+
     def new_output(self, device="cuda"):
         return torch.empty(self.y_ldc_shape or self.out_shape, dtype=self.out_dtype, device=device)
 
     def run(self, x: torch.Tensor, out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
-            stream=None) -> torch.Tensor:
+            stream=None, residual: Optional[torch.Tensor] = None) -> torch.Tensor:
         """Run on x (shape and dtype fixed at creation); the kernels trust the
-        sizes, so they are checked here."""
+        sizes, so they are checked here.  A plan with a fused add
+        (set_residual) takes its residual tensor."""
         _contig(x, "x")
         if tuple(x.shape) != self.in_shape or x.dtype != self.in_dtype:
             raise ValueError(f"x is {tuple(x.shape)} {x.dtype}, the plan expects {self.in_shape} {self.in_dtype}")
@@ -289,6 +311,17 @@ class Plan:
         if self.workspace_size and workspace is not None and workspace.numel() * workspace.element_size() < \
                 self.workspace_size:
             raise ValueError("workspace is smaller than the plan needs")
+        fused = getattr(self, "residual", None)
+        if (fused is None) != (residual is None):
+            raise ValueError("a residual goes with a plan that has a fused add (set_residual), and only with one")
+        if fused is not None:
+            _contig(residual, "residual")
+            if tuple(residual.shape) != fused[0] or residual.dtype != fused[1]:
+                raise ValueError(f"residual is {tuple(residual.shape)} {residual.dtype}, the plan expects "
+                                 f"{fused[0]} {fused[1]}")
+            _check(lib().qnn_plan_run_residual(self._h, _stream(stream), _ptr(x), _ptr(residual), _ptr(out),
+                                               _ptr(workspace)))
+            return out
         _check(lib().qnn_plan_run(self._h, _stream(stream), _ptr(x), _ptr(out), _ptr(workspace)))
         return out
 

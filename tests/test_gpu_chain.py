@@ -5,7 +5,9 @@ hand-off and a qnn.add closing every block, global average pool: 71
 steps); MobileNet-V2's 17 expansion-6 inverted residuals (1x1 expand,
 depthwise 3x3, 1x1 project, residual qnn.add: 58 steps); Inception-v3's
 Mixed 5b and 5c (four branches, average-pool branch, channel concat with
-the block's common quantization: 16 steps)."""
+the block's common quantization: 16 steps).  The ResNet and MobileNet
+chains also run with each residual add fused into the epilogue of the conv
+that qualifies for it, wherever that conv's plan accepts it."""
 import numpy as np
 import pytest
 import torch
@@ -18,12 +20,20 @@ if not torch.cuda.is_available():
     pytest.skip("no GPU", allow_module_level=True)
 
 from gpu_util import Q, O, log, dev, assert_equal  # noqa: E402
+from paper_2006_10226_amd.fusion import residual_fusions  # noqa: E402
 
 
-def run_chain_gpu(ch):
+def run_chain_gpu(ch, fuse=False):
+    """Runs the chain; fuse: residual adds that a conv's plan accepts run in
+    its epilogue (the conv's own output is then never written).  Returns
+    the tensors and the number of fused adds."""
     t = {"x0": dev(ch.x0)}
     keep = []
-    for st in ch.steps:
+    by_conv = {c: (i, r) for i, (c, r) in residual_fusions(ch.graph()).items()} if fuse else {}
+    skip = set()
+    for idx, st in enumerate(ch.steps):
+        if idx in skip:
+            continue
         if isinstance(st, W.ChainConv):
             s_x, zp_x = ch.q[st.src]
             L = st.layer
@@ -39,6 +49,22 @@ def run_chain_gpu(ch):
             else:
                 p = Q.conv2d_plan(shape, "i8", s_x, zp_x, w, st.s_w, st.zp_w, b, L.stride, L.pads,
                                   1, st.s_y, st.zp_y, "i8", st.act)
+            if idx in by_conv:
+                ai, rname = by_conv[idx]
+                add = ch.steps[ai]
+                try:
+                    p.set_residual("i8", *ch.q[rname], add.s_o, add.zp_o, "i8", act=add.act)
+                except Q.QnnError:
+                    pass
+                else:
+                    out = p.new_output()
+                    p.run(t[st.src], out, residual=t[rname])
+                    torch.cuda.synchronize()
+                    log(f"fused {st.dst} + {rname} -> {add.dst}: {p.describe()}")
+                    p.close()
+                    t[add.dst] = out
+                    skip.add(ai)
+                    continue
             if st.y_off is not None and st.dst not in t:
                 t[st.dst] = torch.full(p.y_ldc_shape, 77, dtype=torch.int8, device="cuda")
             out = t[st.dst] if st.y_off is not None else p.new_output()
@@ -53,7 +79,7 @@ def run_chain_gpu(ch):
             s_b, zp_b = ch.q[st.b]
             t[st.dst] = Q.add(t[st.a], s_a, zp_a, t[st.b], s_b, zp_b, st.s_o, st.zp_o, "i8", st.act)
     torch.cuda.synchronize()
-    return {k: v.cpu().numpy() for k, v in t.items()}
+    return {k: v.cpu().numpy() for k, v in t.items()}, len(skip)
 
 
 def run_chain_oracle(ch):
@@ -80,14 +106,26 @@ def run_chain_oracle(ch):
     return t
 
 
-@pytest.mark.parametrize("N", [1, 2])
-def test_resnet50_chain(N):
-    ch = W.resnet50_chain(N)
-    log(f"chain N={N}: {len(ch.steps)} steps")
-    gpu = run_chain_gpu(ch)
-    ref = run_chain_oracle(ch)
+def check_chain(ch, gpu, ref, fused, what):
+    """Every tensor the GPU chain wrote equals the oracle's; with fused
+    adds, only the fused convs' own outputs are missing."""
+    missing = [st.dst for st in ch.steps if st.dst not in gpu]
+    assert len(missing) == fused, missing
     for st in ch.steps:
-        assert_equal(gpu[st.dst], ref[st.dst], f"chain N={N} {st.dst}")
+        if st.dst in gpu:
+            assert_equal(gpu[st.dst], ref[st.dst], f"{what} {st.dst}")
+
+
+@pytest.mark.parametrize("fuse", [False, True])
+@pytest.mark.parametrize("N", [1, 2])
+def test_resnet50_chain(N, fuse):
+    ch = W.resnet50_chain(N)
+    log(f"chain N={N} fuse={fuse}: {len(ch.steps)} steps")
+    gpu, fused = run_chain_gpu(ch, fuse)
+    ref = run_chain_oracle(ch)
+    log(f"  {fused} adds fused")
+    check_chain(ch, gpu, ref, fused, f"chain N={N} fuse={fuse}")
+    assert fuse or fused == 0
     assert len(ch.steps) == 71 and ch.steps[-1].dst == "gap" and ref["gap"].shape == (N, 1, 1, 2048)
     # the data stays informative through the chain: the last block output
     # and the pooled features are neither constant nor all on the clamp
@@ -95,14 +133,15 @@ def test_resnet50_chain(N):
     assert len(np.unique(ref["gap"])) > 20
 
 
+@pytest.mark.parametrize("fuse", [False, True])
 @pytest.mark.parametrize("N", [1, 2])
-def test_mobilenet_v2_chain(N):
+def test_mobilenet_v2_chain(N, fuse):
     ch = W.mobilenet_v2_chain(N)
-    log(f"mobilenet chain N={N}: {len(ch.steps)} steps")
-    gpu = run_chain_gpu(ch)
+    log(f"mobilenet chain N={N} fuse={fuse}: {len(ch.steps)} steps")
+    gpu, fused = run_chain_gpu(ch, fuse)
     ref = run_chain_oracle(ch)
-    for st in ch.steps:
-        assert_equal(gpu[st.dst], ref[st.dst], f"mobilenet chain N={N} {st.dst}")
+    log(f"  {fused} adds fused")
+    check_chain(ch, gpu, ref, fused, f"mobilenet chain N={N} fuse={fuse}")
     assert len(ch.steps) == 58 and ref[ch.steps[-1].dst].shape == (N, 7, 7, 320)
     assert len(np.unique(ref[ch.steps[-1].dst])) > 50
 
@@ -111,10 +150,10 @@ def test_mobilenet_v2_chain(N):
 def test_inception_mixed5_chain(N):
     ch = W.inception_v3_mixed5_chain(N)
     log(f"inception mixed chain N={N}: {len(ch.steps)} steps")
-    gpu = run_chain_gpu(ch)
+    gpu, fused = run_chain_gpu(ch, fuse=True)    # no residual adds: nothing to fuse
     ref = run_chain_oracle(ch)
-    for st in ch.steps:
-        assert_equal(gpu[st.dst], ref[st.dst], f"inception chain N={N} {st.dst}")
+    check_chain(ch, gpu, ref, fused, f"inception chain N={N}")
+    assert fused == 0
     # every channel of both concats was written by a branch (no sentinel left)
     for g, total in (("mixed5b", 256), ("mixed5c", 288)):
         assert ref[g].shape == (N, 35, 35, total)

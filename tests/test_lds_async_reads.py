@@ -2,6 +2,7 @@
 before its registers are touched, on every control-flow path (checked on
 the gfx950 assembly the compiler produces; no GPU needed)."""
 import os
+import re
 import shutil
 import subprocess
 
@@ -73,18 +74,58 @@ def test_checker_loop_carried_read():
     assert len(H.hazards(k)) == 1
 
 
-@pytest.mark.skipif(not shutil.which(HIPCC) and not os.path.exists(HIPCC), reason="hipcc not available")
-@pytest.mark.parametrize("src", ["conv_dma.hip", "conv_wave.hip"])
-def test_kernels_retire_async_lds_reads(src, tmp_path):
-    out = tmp_path / (src + ".s")
-    cmd = [HIPCC, "-x", "hip", "--offload-arch=gfx950", "--cuda-device-only", "-S", "-O3", "-std=c++17",
-           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-mllvm", "-disable-promote-alloca-to-lds", os.path.join(CSRC, src), "-o", str(out)]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    assert r.returncode == 0, r.stderr[-2000:]
-    ks = H.kernels(out.read_text())
+_SOURCES = ["conv_dma.hip", "conv_dma_fused.hip", "conv_tap.hip", "conv_wave.hip", "conv_halo.hip", "conv_window.hip"]
+_ASM = {}
+
+
+def _asm(src, tmp_path_factory):
+    """gfx950 assembly of one source; the first call compiles every source
+    these tests read, side by side."""
+    if not _ASM:
+        d = tmp_path_factory.mktemp("asm")
+        procs = {}
+        for name in _SOURCES:
+            cmd = [HIPCC, "-x", "hip", "--offload-arch=gfx950", "--cuda-device-only", "-S", "-O3", "-std=c++17",
+                   "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
+                   "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                   "-mllvm", "-disable-promote-alloca-to-lds", os.path.join(CSRC, name),
+                   "-o", str(d / (name + ".s"))]
+            procs[name] = subprocess.Popen(cmd, stdout=subprocess.DEVNULL, stderr=subprocess.PIPE, text=True)
+        for name, p in procs.items():
+            err = p.communicate()[1]
+            assert p.returncode == 0, err[-2000:]
+            _ASM[name] = (d / (name + ".s")).read_text()
+    return _ASM[src]
+
+
+needs_hipcc = pytest.mark.skipif(not shutil.which(HIPCC) and not os.path.exists(HIPCC), reason="hipcc not available")
+
+
+@needs_hipcc
+@pytest.mark.parametrize("src", ["conv_dma.hip", "conv_dma_fused.hip", "conv_wave.hip"])
+def test_kernels_retire_async_lds_reads(src, tmp_path_factory):
+    ks = H.kernels(_asm(src, tmp_path_factory))
     assert len(ks) > 0
     bad = {name: H.hazards(lines) for name, lines in ks.items()}
     bad = {k: v for k, v in bad.items() if v}
     assert not bad, {k[:80]: sorted(v.items())[:3] for k, v in bad.items()}
+
+
+@needs_hipcc
+@pytest.mark.parametrize("src", _SOURCES)
+def test_counted_wait_kernels_use_no_scratch(src, tmp_path_factory):
+    # These kernels wait for their staged loads with explicit counts of
+    # outstanding vector-memory operations; a register spill would add
+    # scratch loads and stores to that count and release a wait early.
+    text = _asm(src, tmp_path_factory)
+    sizes = re.findall(r"^\s*\.amdhsa_kernel\s+(\S+)|\.amdhsa_private_segment_fixed_size\s+(\d+)", text, re.M)
+    kernels, name = {}, None
+    for k, size in sizes:
+        if k:
+            name = k
+        elif name is not None:
+            kernels[name] = int(size)
+            name = None
+    assert kernels
+    spilled = {k[:100]: v for k, v in kernels.items() if v}
+    assert not spilled, spilled

@@ -82,6 +82,21 @@ class Chain:
     steps: List[Union[ChainConv, ChainAdd, ChainPool]]
     N: int
 
+    def graph(self):
+        """The steps as (kind, input names, output name): "conv" for a conv
+        writing a whole tensor, "conv_slice" for one writing a concat's
+        channel slice, "dw", "pool" and "add"."""
+        out = []
+        for st in self.steps:
+            if isinstance(st, ChainConv):
+                kind = "dw" if st.layer.depthwise else ("conv" if st.y_off is None else "conv_slice")
+                out.append((kind, (st.src,), st.dst))
+            elif isinstance(st, ChainPool):
+                out.append(("pool", (st.src,), st.dst))
+            else:
+                out.append(("add", (st.a, st.b), st.dst))
+        return out
+
 
 def _f32(v) -> float:
     return float(np.float32(v))
