@@ -356,6 +356,53 @@ def time_warm(items, reps=10):
     return np.array(out)
 
 
+def library_gemm(items, reps=20):
+    """A reference point beside the product, not part of it: the vendor's
+    int8 GEMM (torch._int_mm, hipBLASLt on ROCm) on each conv or dense
+    layer's GEMM shape (M output pixels x K channels x J = R*S*C, J rounded
+    up to a multiple of 8 as the library requires), int32 output, without
+    the gather, zero-point terms or requantize; `reps` calls back to back,
+    replayed from a graph, caches warm.  Returns ms per item (nan for
+    steps that are no GEMM)."""
+    import torch
+    out = []
+    for it in items:
+        if it.kind not in ("conv", "dense") or not it.macs:
+            out.append(float("nan"))
+            continue
+        if it.kind == "dense":
+            M, K = it.layer.M, it.layer.N
+        else:
+            Nb, Ho, Wo, K = it.plan.out_shape
+            M = Nb * Ho * Wo
+        J = -(-(it.macs // (M * K)) // 8) * 8
+        a = torch.randint(-128, 128, (M, J), dtype=torch.int8, device="cuda")
+        b = torch.randint(-128, 128, (K, J), dtype=torch.int8, device="cuda").t()   # column-major J x K
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            torch._int_mm(a, b)
+            torch._int_mm(a, b)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(reps):
+                torch._int_mm(a, b)
+        g.replay()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / reps)
+        out.append(float(np.median(ts)))
+        del g, a, b
+    return np.array(out)
+
+
 def sample_clock(items, graph_step, seconds=2.0, settle=1.0):
     """The GPU's graphics clock while the step runs: steps run back to back
     for `seconds` while a thread reads the current clock (amdsmi, through
@@ -510,6 +557,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="resnet50_b32")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the vendor int8 GEMM (torch._int_mm) on every layer's GEMM shape, warm, "
+                         "as a reference point")
     ap.add_argument("--no-fuse", action="store_true",
                     help="chained workloads: run every residual add as its own kernel")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -582,6 +632,7 @@ def main():
         warm = time_warm(items)
         clock = sample_clock(items, graph if graphed else None)
         log(f"GPU clock while stepping: {clock}")
+    lib_ms = library_gemm(items) if args.library_gemm else np.full(len(items), np.nan)
     groups = {}
     for it, t in zip(items, per):
         g = kernel_group(it)
@@ -642,9 +693,10 @@ def main():
                          "ceiling_frac_of_int8_peak": round(cb_ops / (cb_roof_us * 1e-6) / 1e12 / PEAK_INT8_TOPS, 4),
                          "share_of_step": round(cb_ms / ms, 4)}
     layer_rows = []
-    for it, t, h, tw in zip(items, per, how, warm):
+    for it, t, h, tw, tl in zip(items, per, how, warm, lib_ms):
         row = {"layer": it.name, "kind": it.kind, "plan": it.desc, "us": round(float(t) * 1e3, 3), "timed": h,
                "warm_us": None if np.isnan(tw) else round(float(tw) * 1e3, 3),
+               "library_gemm_us": None if np.isnan(tl) else round(float(tl) * 1e3, 3),
                "gmac": round(it.macs / 1e9, 4), "mbytes": round(it.bytes / 1e6, 3)}
         if it.macs:
             row["tops"] = round(2 * it.macs / (float(t) * 1e-3) / 1e12, 1)
@@ -703,6 +755,13 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if args.library_gemm:
+        gemm = [(float(tl), float(tw)) for tl, tw in zip(lib_ms, warm) if not np.isnan(tl)]
+        out["library_gemm"] = {
+            "what": "torch._int_mm (hipBLASLt) on each conv/dense layer's GEMM shape: int32 output, no gather, "
+                    "zero-point terms or requantize; warm, back to back from a graph",
+            "layers": len(gemm), "us_sum": round(sum(g for g, _ in gemm) * 1e3, 2),
+            "this_library_warm_us_sum": None if args.no_warm_clock else round(sum(w for _, w in gemm) * 1e3, 2)}
     print(json.dumps(out), flush=True)
 
 

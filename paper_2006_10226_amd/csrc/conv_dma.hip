@@ -90,6 +90,47 @@ __global__ void __launch_bounds__(256) pad_image_kernel(const uint8_t *x, int N,
     }
 }
 
+// The same copy for 3-channel images with W % 4 == 0 and a 4-byte aligned
+// x: one wave per padded row (four rows per block); lane t < W / 4 turns
+// source pixels 4t .. 4t + 3 (three aligned dwords) into four padded
+// pixels (the fourth byte zp), the lanes after them fill the pad columns,
+// and rows outside the image are filled whole.
+__global__ void __launch_bounds__(256) pad_rgb_kernel(const uint8_t *x, int N, int H, int W, int Hp, int Wp, int pt,
+                                                      int pl, uint8_t zp, uint8_t *out)
+{
+    const int row = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);   // n * Hp + h
+    if (row >= N * Hp)
+        return;
+    const int lane = (int)(threadIdx.x & 63);
+    const int n = row / Hp, h = row - n * Hp;
+    const int ih = h - pt;
+    const bool row_in = (unsigned)ih < (unsigned)H;
+    const uint32_t fill = 0x01010101u * zp, top = (uint32_t)zp << 24;
+    uint32_t *dst = (uint32_t *)(out + (size_t)row * Wp * 4);
+    const int groups = W >> 2;
+    for (int t = lane; t < groups + (Wp - W); t += 64) {
+        if (t < groups) {
+            uint32_t o0 = fill, o1 = fill, o2 = fill, o3 = fill;
+            if (row_in) {
+                const uint32_t *src = (const uint32_t *)(x + ((size_t)(n * H + ih) * W + 4 * t) * 3);
+                const uint32_t d0 = src[0], d1 = src[1], d2 = src[2];
+                o0 = (d0 & 0xffffffu) | top;
+                o1 = (((d0 >> 24) | (d1 << 8)) & 0xffffffu) | top;
+                o2 = (((d1 >> 16) | (d2 << 16)) & 0xffffffu) | top;
+                o3 = (d2 >> 8) | top;
+            }
+            uint32_t *p = dst + pl + 4 * t;
+            p[0] = o0;
+            p[1] = o1;
+            p[2] = o2;
+            p[3] = o3;
+        } else {
+            const int q = t - groups;        // pad column: the pl left ones, then the right ones
+            dst[q < pl ? q : W + q] = fill;
+        }
+    }
+}
+
 hipError_t launch_rowpack_weights(const int8_t *w, int K, int R, int S, int C, int C4, int Kpad, int Jpad, int8_t *wp,
                                   hipStream_t st)
 {
@@ -107,6 +148,11 @@ hipError_t launch_pad_image(const uint8_t *x, int N, int H, int W, int C, int Hp
         return hipSuccess;
     if (rows >= (1LL << 31))
         return hipErrorInvalidValue;
+    if (C == 3 && C4 == 4 && W % 4 == 0 && ((uintptr_t)x & 3) == 0 && pl >= 0 && Wp >= W + pl) {
+        hipLaunchKernelGGL(pad_rgb_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, x, N, H, W, Hp, Wp, pt,
+                           pl, zp, out);
+        return hipGetLastError();
+    }
     const dim3 grid((unsigned)((Wp + 255) / 256), (unsigned)std::min<long long>(rows, 65535));
     hipLaunchKernelGGL(pad_image_kernel, grid, dim3(256), 0, st, x, N, H, W, C, Hp, Wp, C4, pt, pl, zp, out);
     return hipGetLastError();

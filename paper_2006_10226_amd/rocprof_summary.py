@@ -31,9 +31,9 @@ import os
 import re
 
 _CONV = re.compile(r"conv_mfma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
-_TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)>")
+_TAP = re.compile(r"conv_tap_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+)(?:, ?(true|false))?>")
 _DMA = re.compile(r"conv_dma_kernel<(\d+), ?(\d+), ?(\d+), ?(\d+), ?(\d+), ?(true|false), ?(true|false)"
-                  r"(?:, ?(\d+))?(?:, ?(true|false))?>")
+                  r"(?:, ?(\d+))?(?:, ?(true|false))?(?:, ?(true|false))?>")
 _WAVE = re.compile(r"conv_wave_kernel<(\d+), ?(\d+), ?(true|false)>")
 _HALO = re.compile(r"conv_halo_kernel<(\d+), ?(true|false)>")
 _WIN = re.compile(r"conv_window_kernel<(\d+), ?(\d+), ?(\d+), ?(true|false)>")
@@ -63,15 +63,17 @@ def group_of(kernel_name):
         return f"conv_mfma tile={tc}x{tp}x{bk} gather={avec}"
     m = _TAP.search(kernel_name)
     if m:
-        tc, tp, bk, wc, wp = (int(v) for v in m.groups())
-        return f"conv_tap tile={tc}x{tp}x{bk} threads={wc * wp * 64} stages=2"
+        tc, tp, bk, wc, wp = (int(v) for v in m.groups()[:5])
+        fused = " +add" if m.group(6) == "true" else ""
+        return f"conv_tap tile={tc}x{tp}x{bk} threads={wc * wp * 64} stages=2{fused}"
     m = _DMA.search(kernel_name)
     if m:
         tc, tp, wc, wp, ns = (int(v) for v in m.groups()[:5])
         short = "s" if m.group(7) == "true" else ""
         ks = int(m.group(8)) if m.group(8) else 1
         split = " ksplit" if m.group(9) == "true" else ""
-        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * ks * 64} stages={ns}{short}{split}"
+        fused = " +add" if m.group(10) == "true" else ""
+        return f"conv_dma tile={tc}x{tp}x64 threads={wc * wp * ks * 64} stages={ns}{short}{split}{fused}"
     m = _WAVE.search(kernel_name)
     if m:
         split = int(m.group(1))

@@ -614,6 +614,8 @@ def test_every_wave_split(split):
     (W.ConvLayer("stem", 29, 31, 3, 64, 7, 7, 2, (3, 3, 3, 3)), 3),
     (W.ConvLayer("stem3", 35, 33, 3, 32, 3, 3, 2, (0, 0, 0, 0)), 2),
     (W.ConvLayer("stem3p", 20, 20, 3, 40, 3, 3, 1, (1, 2, 0, 1)), 2),
+    (W.ConvLayer("stem4", 29, 32, 3, 64, 7, 7, 2, (3, 3, 3, 3)), 3),     # RGB rows of whole dwords
+    (W.ConvLayer("stem4n", 10, 24, 3, 16, 3, 3, 1, (0, 0, 0, 0)), 2),    # padded rows wider than the image
     (W.ConvLayer("c8", 17, 16, 8, 24, 3, 3, 1, (1, 1, 1, 1)), 2),
     (W.ConvLayer("c4_5x5", 15, 15, 4, 70, 5, 5, 2, (2, 2, 2, 2)), 2),
     (W.ConvLayer("c1_5x5", 27, 27, 1, 20, 5, 5, 2, (2, 1, 2, 1)), 2),
