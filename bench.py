@@ -110,12 +110,13 @@ CHAINS = {
 }
 
 
-def setup_chain(workload, fuse=True):
+def setup_chain(workload, fuse=True, tensors=None):
     """Plans and device tensors of a chained network: every step writes its
     own output tensor (or its channel slice of a concat), which its
     consumers read.  fuse: each residual add that a conv's plan can run in
     its epilogue (paper_2006_10226_amd.fusion) runs there, and the conv's
-    own output is never written."""
+    own output is never written.  tensors: a dict that receives the chain's
+    device tensors by name (for tests)."""
     import torch
     import workloads as W
     from paper_2006_10226_amd import qnn as Q
@@ -191,6 +192,8 @@ def setup_chain(workload, fuse=True):
             it.run = (lambda it=it: Q.add(it.a, it.args[0], it.args[1], it.b, it.args[2], it.args[3], it.args[4],
                                           it.args[5], "i8", it.args[6], out=it.out))
         items.append(it)
+    if tensors is not None:
+        tensors.update(t)
     return items, N
 
 

@@ -159,3 +159,24 @@ def test_inception_mixed5_chain(N):
         assert ref[g].shape == (N, 35, 35, total)
         assert not (gpu[g] == 77).all(axis=(0, 1, 2)).any(), g
     assert len(np.unique(ref["mixed5c"])) > 50
+
+
+@pytest.mark.parametrize("workload,fn", [("resnet50_b32_chain", "resnet50_chain"),
+                                         ("mobilenet_v2_b64_chain", "mobilenet_v2_chain")])
+def test_chain_as_benchmarked(workload, fn):
+    """The chained workloads at their benchmark batch, set up and run
+    exactly as bench.py times them (its plans, tensors and fused adds): every
+    tensor the step writes, byte for byte, against the oracle's chain."""
+    import bench
+    t = {}
+    items, N = bench.setup_chain(workload, fuse=True, tensors=t)
+    for it in items:
+        it.run()
+    torch.cuda.synchronize()
+    fused = sum(1 for it in items if getattr(it, "residual", None) is not None)
+    log(f"{workload}: {len(items)} launches, {fused} adds fused")
+    ch = getattr(W, fn)(N)
+    ref = run_chain_oracle(ch)
+    gpu = {k: v.cpu().numpy() for k, v in t.items()}
+    check_chain(ch, gpu, ref, fused, workload)
+    assert fused > 0
