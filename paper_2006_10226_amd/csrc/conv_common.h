@@ -63,27 +63,45 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
     return packed;
 }
 
-// Residual qnn.add fused into the epilogue: 16 requantized output bytes
-// (channels k0 .. k0 + n - 1 of pixel m, n <= 16; dtype ydt) and the
-// residual bytes of the same elements go through add_one; the add's bytes
-// replace the outputs (those past n are not stored).
-__device__ __forceinline__ v4i residual_add16(const ConvArgs &a, v4i v, int m, int k0, int n)
+// Residual qnn.add fused into the epilogue.  The staged copy-out hands
+// thread tid the 16-byte chunks idx = it * NT + tid (it < ITERS) of the
+// tile: pixel row idx / CH, channels 16 * (idx % CH) on; the residual
+// chunks of the same elements are loaded at the start of the epilogue
+// (residual_prefetch), so that their memory latency overlaps the
+// requantize and the staging.
+
+// Residual bytes of one chunk (n <= 16 channels from k0 at pixel m): a
+// 16-byte load where rows are 16-byte aligned and the chunk is whole,
+// else byte loads (then `vec` is false and the caller loads later).
+__device__ __forceinline__ bool residual_chunk_vec(const ConvArgs &a, int n)
 {
-    const uint8_t *rp = a.res + (size_t)m * a.r_ldc + a.r_coff + k0;
-    uint32_t r[4] = {0u, 0u, 0u, 0u};
-    if (a.res_vec && n == 16) {
-        const v4i t = __builtin_nontemporal_load((const v4i *)rp);
+    return a.res_vec && n == 16;
+}
+
+template <int TC, int TP, int NT>
+__device__ __forceinline__ void residual_prefetch(const ConvArgs &a, int c0, int p0,
+                                                  v4i (&r)[(TP * (TC / 16) + NT - 1) / NT])
+{
+    constexpr int CH = TC / 16, ITERS = (TP * CH + NT - 1) / NT;
+    const int kmax = a.K - c0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-            r[e] = (uint32_t)t[e];
-    } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-            if (e < n)
-                r[e >> 2] |= (uint32_t)rp[e] << (8 * (e & 3));
+    for (int it = 0; it < ITERS; ++it) {
+        const int idx = it * NT + (int)threadIdx.x;
+        const int pl = idx / CH, qc = idx % CH;
+        const int m = p0 + pl;
+        r[it] = v4i{0, 0, 0, 0};
+        if (idx < TP * CH && m < a.M && qc * 16 < kmax && residual_chunk_vec(a, min(16, kmax - qc * 16)))
+            r[it] = __builtin_nontemporal_load(
+                (const v4i *)(a.res + (size_t)m * a.r_ldc + a.r_coff + c0 + qc * 16));
     }
-    // one 4-byte word per pass, the words rotated through position 0 (a
-    // rolled loop keeps a single copy of add_one's code)
+}
+
+// The add of 16 requantized output bytes v (channels k0 .. k0 + n - 1 of
+// pixel m, dtype ydt) and their residual bytes r (rdt); the sum's bytes
+// replace the outputs.  One 4-byte word per pass, the words rotated through
+// position 0 (a rolled loop keeps a single copy of add_one's code).
+__device__ __forceinline__ v4i residual_add16(const ConvArgs &a, v4i v, v4i r)
+{
     v4i o = v4i{0, 0, 0, 0};
 #pragma unroll 1
     for (int q = 0; q < 4; ++q) {
@@ -91,36 +109,44 @@ __device__ __forceinline__ v4i residual_add16(const ConvArgs &a, v4i v, int m, i
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const uint32_t xb = ((uint32_t)v[0] >> (8 * e)) & 0xffu;
-            const uint32_t rb = (r[0] >> (8 * e)) & 0xffu;
+            const uint32_t rb = ((uint32_t)r[0] >> (8 * e)) & 0xffu;
             const int x = a.ydt == 1 ? (int)(int8_t)xb : (int)xb;
             const int y = a.rdt == 1 ? (int)(int8_t)rb : (int)rb;
             ow |= ((uint32_t)add_one(a.fadd, x, y) & 0xffu) << (8 * e);
         }
         o = v4i{o[1], o[2], o[3], (int)ow};
         v = v4i{v[1], v[2], v[3], v[0]};
-        const uint32_t r0 = r[0];
-        r[0] = r[1];
-        r[1] = r[2];
-        r[2] = r[3];
-        r[3] = r0;
+        r = v4i{r[1], r[2], r[3], r[0]};
     }
     return o;
 }
 
 // Copy-out of a staged tile (TP pixel rows of SP bytes in LDS, the tile's
-// first min(TC, kmax) channels valid) with the residual add applied (a
-// rolled loop: the add's code is long and runs once per tile).
+// first min(TC, kmax) channels valid) with the residual add applied, the
+// residual chunks prefetched in r (byte loads here where they were not).
 template <int TC, int TP, int NT, int SP>
-__device__ __forceinline__ void copy_out_residual(const ConvArgs &a, const int8_t *stage, int c0, int p0, int kmax)
+__device__ __forceinline__ void copy_out_residual(const ConvArgs &a, const int8_t *stage, int c0, int p0, int kmax,
+                                                  const v4i (&r)[(TP * (TC / 16) + NT - 1) / NT])
 {
-    constexpr int CH = TC / 16;
-#pragma unroll 1
-    for (int idx = threadIdx.x; idx < TP * CH; idx += NT) {
+    constexpr int CH = TC / 16, ITERS = (TP * CH + NT - 1) / NT;
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+        const int idx = it * NT + (int)threadIdx.x;
         const int pl = idx / CH, qc = idx % CH;
         const int m = p0 + pl;
-        if (m < a.M && qc * 16 < kmax) {
+        if (idx < TP * CH && m < a.M && qc * 16 < kmax) {
             const int n = min(16, kmax - qc * 16);
-            const v4i v = residual_add16(a, *(const v4i *)(stage + pl * SP + qc * 16), m, c0 + qc * 16, n);
+            v4i rv = r[it];
+            if (!residual_chunk_vec(a, n)) {
+                const uint8_t *rp = a.res + (size_t)m * a.r_ldc + a.r_coff + c0 + qc * 16;
+                uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    if (e < n)
+                        w[e >> 2] |= (uint32_t)rp[e] << (8 * (e & 3));
+                rv = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+            }
+            const v4i v = residual_add16(a, *(const v4i *)(stage + pl * SP + qc * 16), rv);
             uint8_t *dst = (uint8_t *)a.y + (size_t)m * a.y_ldc + a.y_coff + c0 + qc * 16;
             if (n == 16) {
                 __builtin_nontemporal_store(v, (v4i *)dst);
@@ -165,6 +191,14 @@ __device__ __forceinline__ void lds_settled(v4i (&f)[F])
         asm volatile("" : "+v"(f[i]));
 }
 
+// One channel record of the tile's records in LDS, read through an LDS
+// pointer (a generic pointer would make it a flat load, which also waits
+// for every global load in flight).
+__device__ __forceinline__ v4i lds_rec(const ChanRec *p)
+{
+    return *(const __attribute__((address_space(3))) v4i *)(const __attribute__((address_space(3))) void *)p;
+}
+
 // Adds bconst (bias and terms 2 and 4) of each block's four channels to the
 // accumulators of a WC x WP wave grid, from the tile's records in LDS (the
 // epilogue then leaves bconst out of the requantize).  ASYNC: the records
@@ -198,7 +232,8 @@ __device__ __forceinline__ void add_bconst(v4i (&acc)[TC / WC / 16][TP / WP / 16
 #pragma unroll
         for (int i = 0; i < FC; ++i) {
             const int cl = wc * WTC + i * 16 + (lane >> 4) * 4;
-            const v4i b = v4i{recs[cl].bconst, recs[cl + 1].bconst, recs[cl + 2].bconst, recs[cl + 3].bconst};
+            const v4i b = v4i{lds_rec(recs + cl).y, lds_rec(recs + cl + 1).y, lds_rec(recs + cl + 2).y,
+                              lds_rec(recs + cl + 3).y};
 #pragma unroll
             for (int j = 0; j < FP; ++j)
                 acc[i][j] += b;
@@ -213,14 +248,13 @@ __device__ __forceinline__ void add_bconst(v4i (&acc)[TC / WC / 16][TP / WP / 16
 // taps outside the image) and term 3, then requantizes and stores, through
 // `stage` (LDS, at least TP * (TC + 16) bytes when a.staged) as whole
 // 16-byte pixel-row chunks, or directly.  Every wave must be past its last
-// read of `stage` before the call.  `recs`, when given, holds the tile's
-// channel records (channels c0 .. c0 + TC - 1) in LDS, else they are read
-// from a.chan; with `recs` the accumulators already hold bconst (see
-// add_bconst).  FUSE: the staged copy-out applies the residual add (the
+// read of `stage` before the call.  `recs` holds the tile's channel
+// records (channels c0 .. c0 + TC - 1) in LDS, and the accumulators
+// already hold bconst (see add_bconst).  FUSE: the staged copy-out applies the residual add (the
 // host launches these instantiations only with a.res set and a.staged).
 template <int TC, int TP, int WC, int WP, int STAGE_BYTES, bool FUSE = false>
 __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC / 16][TP / WP / 16], int8_t *stage,
-                                           int c0, int p0, const ChanRec *recs = nullptr)
+                                           int c0, int p0, const ChanRec *recs)
 {
     constexpr int NT = WC * WP * 64;
     constexpr int WTC = TC / WC, WTP = TP / WP;
@@ -232,6 +266,9 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
     const int wc = wave / WP, wpos = wave % WP;
     const int lrow = lane & 15, lchk = lane >> 4;
     const int mb = p0 + wpos * WTP + lrow;
+    v4i rres[FUSE ? (TP * (TC / 16) + NT - 1) / NT : 1];
+    if constexpr (FUSE)
+        residual_prefetch<TC, TP, NT>(a, c0, p0, rres);
 
     if (a.pcorr) {
         // taps outside the image were gathered as x = 0; the padding value
@@ -272,9 +309,8 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
 #pragma unroll
             for (int e = 0; e < 4; ++e)
             {
-                rec[e] = *(const v4i *)(recs ? recs + cl + e : a.chan + c0 + cl + e);
-                if (recs)
-                    rec[e].y = 0;
+                rec[e] = lds_rec(recs + cl + e);
+                rec[e].y = 0;
             }
 #pragma unroll
             for (int j = 0; j < FP; ++j) {
@@ -286,7 +322,7 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
         constexpr int CH = TC / 16;
         const int kmax = a.K - c0;
         if constexpr (FUSE) {
-            copy_out_residual<TC, TP, NT, SP>(a, stage, c0, p0, kmax);
+            copy_out_residual<TC, TP, NT, SP>(a, stage, c0, p0, kmax, rres);
             return;
         }
 #pragma unroll
@@ -319,9 +355,8 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
 #pragma unroll
         for (int e = 0; e < 4; ++e)
         {
-            rec[e] = *(const v4i *)(recs ? recs + (ch - c0) + e : a.chan + ch + e);
-            if (recs)
-                rec[e].y = 0;
+            rec[e] = lds_rec(recs + (ch - c0) + e);
+            rec[e].y = 0;
         }
 #pragma unroll
         for (int j = 0; j < FP; ++j) {
