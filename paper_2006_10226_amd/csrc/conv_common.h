@@ -121,12 +121,48 @@ __device__ __forceinline__ v4i residual_add16(const ConvArgs &a, v4i v, v4i r)
     return o;
 }
 
+typedef __attribute__((address_space(3))) int32_t lds_i32;
+
+// The add with the term tables in LDS (AddArgs::tab copied there): each
+// element is clamp(tab[x] + tab[256 + r]).
+__device__ __forceinline__ v4i residual_add16_tab(const ConvArgs &a, v4i v, v4i r, const lds_i32 *tab)
+{
+    v4i o;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        uint32_t ow = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t xb = ((uint32_t)v[w] >> (8 * e)) & 0xffu;
+            const uint32_t rb = ((uint32_t)r[w] >> (8 * e)) & 0xffu;
+            const int t = clamp_i32(tab[xb] + tab[256 + rb], a.fadd.lo, a.fadd.hi);
+            ow |= ((uint32_t)t & 0xffu) << (8 * e);
+        }
+        o[w] = (int)ow;
+    }
+    return o;
+}
+
+// LDS home of the term tables in the fused instantiations.
+template <bool FUSE>
+__device__ __forceinline__ lds_i32 *fuse_tables()
+{
+    if constexpr (FUSE) {
+        __shared__ __attribute__((aligned(16))) int32_t tab[512];
+        return (lds_i32 *)tab;
+    } else {
+        return nullptr;
+    }
+}
+
 // Copy-out of a staged tile (TP pixel rows of SP bytes in LDS, the tile's
 // first min(TC, kmax) channels valid) with the residual add applied, the
-// residual chunks prefetched in r (byte loads here where they were not).
+// residual chunks prefetched in r (byte loads here where they were not);
+// tab: the term tables in LDS, or nullptr for the add's own arithmetic.
 template <int TC, int TP, int NT, int SP>
 __device__ __forceinline__ void copy_out_residual(const ConvArgs &a, const int8_t *stage, int c0, int p0, int kmax,
-                                                  const v4i (&r)[(TP * (TC / 16) + NT - 1) / NT])
+                                                  const v4i (&r)[(TP * (TC / 16) + NT - 1) / NT],
+                                                  const lds_i32 *tab)
 {
     constexpr int CH = TC / 16, ITERS = (TP * CH + NT - 1) / NT;
 #pragma unroll
@@ -146,7 +182,8 @@ __device__ __forceinline__ void copy_out_residual(const ConvArgs &a, const int8_
                         w[e >> 2] |= (uint32_t)rp[e] << (8 * (e & 3));
                 rv = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
             }
-            const v4i v = residual_add16(a, *(const v4i *)(stage + pl * SP + qc * 16), rv);
+            const v4i sv = *(const v4i *)(stage + pl * SP + qc * 16);
+            const v4i v = tab ? residual_add16_tab(a, sv, rv, tab) : residual_add16(a, sv, rv);
             uint8_t *dst = (uint8_t *)a.y + (size_t)m * a.y_ldc + a.y_coff + c0 + qc * 16;
             if (n == 16) {
                 __builtin_nontemporal_store(v, (v4i *)dst);
@@ -267,8 +304,16 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
     const int lrow = lane & 15, lchk = lane >> 4;
     const int mb = p0 + wpos * WTP + lrow;
     v4i rres[FUSE ? (TP * (TC / 16) + NT - 1) / NT : 1];
-    if constexpr (FUSE)
+    int32_t tabv[FUSE ? 512 / NT : 1];
+    if constexpr (FUSE) {
+        static_assert(512 % NT == 0, "the term tables split evenly over the threads");
         residual_prefetch<TC, TP, NT>(a, c0, p0, rres);
+        if (a.fadd.tab) {
+#pragma unroll
+            for (int i = 0; i < 512 / NT; ++i)
+                tabv[i] = a.fadd.tab[i * NT + tid];
+        }
+    }
 
     if (a.pcorr) {
         // taps outside the image were gathered as x = 0; the padding value
@@ -318,11 +363,19 @@ __device__ __forceinline__ void store_tile(const ConvArgs &a, v4i (&acc)[TC / WC
                 *(uint32_t *)(stage + pl * SP + cl) = requant4(a, acc[i][j], rec);
             }
         }
+        if constexpr (FUSE) {
+            if (a.fadd.tab) {
+#pragma unroll
+                for (int i = 0; i < 512 / NT; ++i)
+                    fuse_tables<FUSE>()[i * NT + tid] = tabv[i];
+            }
+        }
         __syncthreads();
         constexpr int CH = TC / 16;
         const int kmax = a.K - c0;
         if constexpr (FUSE) {
-            copy_out_residual<TC, TP, NT, SP>(a, stage, c0, p0, kmax, rres);
+            copy_out_residual<TC, TP, NT, SP>(a, stage, c0, p0, kmax, rres,
+                                              a.fadd.tab ? fuse_tables<FUSE>() : nullptr);
             return;
         }
 #pragma unroll

@@ -297,6 +297,25 @@ hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned,
     return hipGetLastError();
 }
 
+// AddArgs::tab of a fused residual add: thread b of 256 writes the term of
+// the byte b as the first operand (dtype adt) and, plus zp_y, as the
+// second (bdt).  The plan builds it only where every term, and so every
+// sum, fits 32 bits.
+__global__ void __launch_bounds__(256) add_table_kernel(AddArgs a, int adt, int bdt, int32_t *tab)
+{
+    const int b = (int)threadIdx.x;
+    const int x = adt == 1 ? (int)(int8_t)b : b;
+    const int y = bdt == 1 ? (int)(int8_t)b : b;
+    tab[b] = (int32_t)add_term_a(a, x);
+    tab[256 + b] = (int32_t)(add_term_b(a, y) + a.zp_y);
+}
+
+hipError_t launch_add_table(const AddArgs &a, int adt, int bdt, int32_t *tab, hipStream_t st)
+{
+    hipLaunchKernelGGL(add_table_kernel, dim3(1), dim3(256), 0, st, a, adt, bdt, tab);
+    return hipGetLastError();
+}
+
 // Reads n16 16-byte words of `buf` (grid-stride) so that the L2s and the
 // last-level cache hold clean lines of it; `sink` receives a value only in
 // the impossible case of an all-ones sum, which keeps the loads alive.

@@ -166,6 +166,7 @@ struct qnn_plan {
     int32_t y_zp = 0;
     int y_dt = QNN_UINT8;
     bool fused = false;
+    int32_t *addtab = nullptr;  // the fused add's term tables (AddArgs::tab), plan-owned
     size_t ws_asum_bytes = 0, ws_xpad_bytes = 0;
     size_t ws_cnt_bytes = 0, ws_part_bytes = 0;   // split reduction: counters, partial sums
     int32_t C_in = 0;           // channels of the caller's x (before padding to a.C)
@@ -196,6 +197,8 @@ void free_plan(qnn_plan *p)
         (void)hipFree(p->dev);
     if (p->ws_own)
         (void)hipFree(p->ws_own);
+    if (p->addtab)
+        (void)hipFree(p->addtab);
     delete p;
 }
 
@@ -1949,12 +1952,37 @@ qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams 
     qnn_status s = make_add_args((qnn_dtype)plan->y_dt, y_q, r_dtype, r_q, o_dtype, o_q, act, rounding, &args);
     if (s != QNN_OK)
         return s;
+    // Term tables (one term per operand byte): exact when every term, and
+    // so every sum, fits 32 bits.  A term is round((v - zp) * m / 2^n) with
+    // |v - zp| at most that of the dtype's ends, within 2 of the real product.
+    auto term_bound = [](qnn_dtype dt, int32_t zp, int32_t m, int32_t n) {
+        const double lo = dt == QNN_INT8 ? -128.0 : 0.0, hi = dt == QNN_INT8 ? 127.0 : 255.0;
+        const double v = std::max(std::fabs(lo - zp), std::fabs(hi - zp));
+        return v * (double)m / std::ldexp(1.0, n) + 2.0;
+    };
+    const double bound = term_bound((qnn_dtype)plan->y_dt, args.zpa, args.ma, args.na) +
+                         term_bound(r_dtype, args.zpb, args.mb, args.nb) + std::fabs((double)args.zp_y);
+    if (bound < std::ldexp(1.0, 30)) {
+        hipError_t e;
+        if ((e = hipMalloc((void **)&plan->addtab, 512 * sizeof(int32_t))) != hipSuccess) {
+            plan->addtab = nullptr;
+            return hip_fail(e, "plan_set_residual: table allocation");
+        }
+        if ((e = launch_add_table(args, plan->y_dt == QNN_INT8 ? 1 : 0, r_dtype == QNN_INT8 ? 1 : 0, plan->addtab,
+                                  nullptr)) != hipSuccess ||
+            (e = hipStreamSynchronize(nullptr)) != hipSuccess) {
+            (void)hipFree(plan->addtab);
+            plan->addtab = nullptr;
+            return hip_fail(e, "plan_set_residual: table kernel");
+        }
+        args.tab = plan->addtab;
+    }
     plan->conv.fadd = args;
     plan->conv.r_ldc = r_ldc;
     plan->conv.r_coff = r_coff;
     plan->conv.rdt = r_dtype == QNN_INT8 ? 1 : 0;
     plan->fused = true;
-    plan->desc += " +add";
+    plan->desc += args.tab ? " +add" : " +add(no-tables)";
     return QNN_OK;
 }
 

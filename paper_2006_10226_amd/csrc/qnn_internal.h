@@ -111,6 +111,12 @@ struct AddArgs {
     // np = shift - 16, c = 2^(np - 1)); the operands are 8-bit, so the
     // zero-point-adjusted values fit 9 bits
     int32_t fast, mah, mal, npa, ca, mbh, mbl, npb, cb;
+    // fused residual add only: tab[b] = add_term_a of the byte b read as
+    // the conv output's dtype, tab[256 + b] = add_term_b of the byte b read
+    // as the residual's dtype, plus zp_y (512 int32 in device memory, built
+    // by add_table_kernel), so that an element's sum is clamp(tab[x] +
+    // tab[256 + r]); nullptr where a 32-bit sum could overflow
+    const int32_t *tab;
 };
 
 // round(v * mult / 2^shift), ties up, for |v| < 2^9 and shift = np + 16 with
@@ -124,18 +130,28 @@ __device__ __forceinline__ int round_mul_shift_small(int v, int mh, int ml, int 
     return (__mul24(v, mh) + c + (__mul24(v, ml) >> 16)) >> np;
 }
 
-// One element of qnn.add: each operand requantized to the output scale
-// (x - zp_a) * Ma, (y - zp_b) * Mb, summed, zp_y added, clamped.
+// The two terms of qnn.add: each operand requantized to the output scale,
+// round((x - zp_a) * Ma) and round((y - zp_b) * Mb).
+__device__ __forceinline__ long long add_term_a(const AddArgs &a, int x)
+{
+    if (a.fast)
+        return round_mul_shift_small(x - a.zpa, a.mah, a.mal, a.npa, a.ca);
+    return rounding_mul_shift<true>(x - a.zpa, a.ma, a.na, a.rounding);
+}
+__device__ __forceinline__ long long add_term_b(const AddArgs &a, int y)
+{
+    if (a.fast)
+        return round_mul_shift_small(y - a.zpb, a.mbh, a.mbl, a.npb, a.cb);
+    return rounding_mul_shift<true>(y - a.zpb, a.mb, a.nb, a.rounding);
+}
+
+// One element of qnn.add: the two terms summed, zp_y added, clamped (the
+// 24-bit form in 32-bit arithmetic, whose terms fit 2^24).
 __device__ __forceinline__ int add_one(const AddArgs &a, int x, int y)
 {
-    if (a.fast) {
-        const int t = round_mul_shift_small(x - a.zpa, a.mah, a.mal, a.npa, a.ca) +
-                      round_mul_shift_small(y - a.zpb, a.mbh, a.mbl, a.npb, a.cb);
-        return clamp_i32(t + a.zp_y, a.lo, a.hi);
-    }
-    const long long t = rounding_mul_shift<true>(x - a.zpa, a.ma, a.na, a.rounding) +
-                        rounding_mul_shift<true>(y - a.zpb, a.mb, a.nb, a.rounding);
-    return clampll(t + a.zp_y, a.lo, a.hi);
+    if (a.fast)
+        return clamp_i32((int)add_term_a(a, x) + (int)add_term_b(a, y) + a.zp_y, a.lo, a.hi);
+    return clampll(add_term_a(a, x) + add_term_b(a, y) + a.zp_y, a.lo, a.hi);
 }
 
 // Largest wave tile (channels x pixels of one wave) whose epilogue holds
@@ -396,6 +412,8 @@ hipError_t launch_requantize(const ReqArgs &a, int xdt, int ydt, bool aligned, h
 hipError_t launch_cache_sweep(const void *buf, size_t bytes, int *sink, hipStream_t st);
 hipError_t launch_flip_bytes(const uint8_t *in, uint8_t *out, size_t n, hipStream_t st);
 hipError_t launch_add(const AddArgs &a, int adt, int bdt, int ydt, bool aligned, hipStream_t st);
+// Builds AddArgs::tab (512 int32) for operand dtypes adt and bdt (0 uint8, 1 int8).
+hipError_t launch_add_table(const AddArgs &a, int adt, int bdt, int32_t *tab, hipStream_t st);
 
 // Quantized pool2d (Eq. (4)): NHWC input and output of one dtype; mode 0
 // average (rounding 0 HALF_UP, 1 HALF_AWAY; count_pad counts padded cells

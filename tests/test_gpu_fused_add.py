@@ -59,6 +59,29 @@ def test_fused_add_matches_conv_then_add(i, dts):
         assert_equal(y.cpu().numpy()[..., :layer.Cout], ref, f"fused add {layer.name} {dts} {rounding}")
 
 
+def test_fused_add_term_tables_and_without():
+    """The epilogue adds through the plan's per-byte term tables wherever a
+    32-bit sum of two terms cannot overflow, and through the add's own
+    64-bit arithmetic where it can (a residual scale 10^7 times the
+    output's); both byte-exact."""
+    layer = W.ConvLayer("t1x1", 6, 9, 64, 64, 1, 1, 1, (0, 0, 0, 0))
+    c = W.conv_case(layer, 2, seed=31)
+    mid = run_oracle(c)
+    for s_r, s_o, zp_r, zp_o, tables in ((0.02, 0.03, 130, 128, True), (4096.0, 0.0004096, 5, 100, False),
+                                         (0.0004096, 4096.0, 250, 7, True)):
+        full, r = _residual(mid.shape, "u8", seed=9)
+        ref = O.add(mid, c.s_y, c.zp_y, r, s_r, zp_r, s_o, zp_o, "u8", None)
+        with env(QNN_DMA=15):
+            p, keep = make_plan(c)
+        p.set_residual("u8", s_r, zp_r, s_o, zp_o, "u8")
+        d = p.describe()
+        assert d.endswith(" +add") == tables and d.endswith("+add(no-tables)") != tables, d
+        y = p.run(dev(c.x), residual=dev(full))
+        torch.cuda.synchronize()
+        p.close()
+        assert_equal(y.cpu().numpy(), ref, f"fused add scales {s_r} {s_o}: {d}")
+
+
 @pytest.mark.parametrize("r_geom,y_geom", [((96, 16), (96, 0)), ((101, 5), (96, 16)), ((80, 0), (112, 32)),
                                             ((67, 3), (64, 0))])
 def test_fused_add_slices(r_geom, y_geom):
