@@ -428,23 +428,36 @@ __global__ void __launch_bounds__(WC *WP * 64 * KS, (KS > 1 ? 1 : dma_occupancy<
                 return;
             if (tid == 0)
                 __hip_atomic_store(a.cnt + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            for (int q = 0; q < S; ++q) {
-                if (q == part)
-                    continue;
-                const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
-                    (void *)((char *)a.part + ((size_t)tile * S + q) * SLOT), (short)0, SLOT, kBufFlags);
-                v4i t[FC][FP];
+            // the other parts' partial tiles, QB of them loaded at once so
+            // that their memory latencies overlap (QB bounded by registers)
+            constexpr int QB = FC * FP >= 16 ? 1 : 16 / (FC * FP);
+            for (int q0 = 0; q0 < S; q0 += QB) {
+                v4i t[QB][FC][FP];
 #pragma unroll
-                for (int i = 0; i < FC; ++i)
+                for (int u = 0; u < QB; ++u) {
+                    const int q = q0 + u;
+                    if (q < S && q != part) {
+                        const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+                            (void *)((char *)a.part + ((size_t)tile * S + q) * SLOT), (short)0, SLOT, kBufFlags);
 #pragma unroll
-                    for (int j = 0; j < FP; ++j)
-                        t[i][j] = __builtin_amdgcn_raw_buffer_load_b128(rq, (((wave * FC + i) * FP + j) * 64 + lane) * 16,
-                                                                       0, kAgentScope);
+                        for (int i = 0; i < FC; ++i)
 #pragma unroll
-                for (int i = 0; i < FC; ++i)
+                            for (int j = 0; j < FP; ++j)
+                                t[u][i][j] = __builtin_amdgcn_raw_buffer_load_b128(
+                                    rq, (((wave * FC + i) * FP + j) * 64 + lane) * 16, 0, kAgentScope);
+                    }
+                }
 #pragma unroll
-                    for (int j = 0; j < FP; ++j)
-                        acc[i][j] += t[i][j];
+                for (int u = 0; u < QB; ++u) {
+                    const int q = q0 + u;
+                    if (q < S && q != part) {
+#pragma unroll
+                        for (int i = 0; i < FC; ++i)
+#pragma unroll
+                            for (int j = 0; j < FP; ++j)
+                                acc[i][j] += t[u][i][j];
+                    }
+                }
             }
         }
         if constexpr (KS > 1) {
