@@ -162,7 +162,8 @@ def test_inception_mixed5_chain(N):
 
 
 @pytest.mark.parametrize("workload,fn", [("resnet50_b32_chain", "resnet50_chain"),
-                                         ("mobilenet_v2_b64_chain", "mobilenet_v2_chain")])
+                                         ("mobilenet_v2_b64_chain", "mobilenet_v2_chain"),
+                                         ("inception_v3_mixed5_b64_chain", "inception_v3_mixed5_chain")])
 def test_chain_as_benchmarked(workload, fn):
     """The chained workloads at their benchmark batch, set up and run
     exactly as bench.py times them (its plans, tensors and fused adds): every
@@ -179,4 +180,4 @@ def test_chain_as_benchmarked(workload, fn):
     ref = run_chain_oracle(ch)
     gpu = {k: v.cpu().numpy() for k, v in t.items()}
     check_chain(ch, gpu, ref, fused, workload)
-    assert fused > 0
+    assert fused > 0 or fn == "inception_v3_mixed5_chain"   # Inception blocks have no residual adds
