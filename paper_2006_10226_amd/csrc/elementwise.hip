@@ -214,9 +214,19 @@ __global__ void __launch_bounds__(256) requantize_kernel(ReqArgs a)
     }
 }
 
+// With a.tab_ok each workgroup first tabulates the two terms for every
+// operand byte in LDS (256 threads, one byte each), and an element is then
+// clamp(tab[a] + tab[256 + b]).
 template <int ADT, int BDT, int YDT, bool VEC>
 __global__ void __launch_bounds__(256) add_kernel(AddArgs a)
 {
+    __shared__ int32_t tab[512];
+    if (a.tab_ok) {
+        const int b = (int)threadIdx.x;
+        tab[b] = (int32_t)add_term_a(a, ADT == 1 ? (int)(int8_t)b : b);
+        tab[256 + b] = (int32_t)(add_term_b(a, BDT == 1 ? (int)(int8_t)b : b) + a.zp_y);
+        __syncthreads();
+    }
     const long long ngroups = (a.count + 15) / 16;
     const long long stride = (long long)gridDim.x * blockDim.x;
     for (long long g = (long long)blockIdx.x * blockDim.x + threadIdx.x; g < ngroups; g += stride) {
@@ -225,9 +235,15 @@ __global__ void __launch_bounds__(256) add_kernel(AddArgs a)
             int u[16], v[16];
             ld16<ADT>(a.a, i0, u);
             ld16<BDT>(a.b, i0, v);
+            if (a.tab_ok) {
 #pragma unroll
-            for (int k = 0; k < 16; ++k)
-                u[k] = add_one(a, u[k], v[k]);
+                for (int k = 0; k < 16; ++k)
+                    u[k] = clamp_i32(tab[u[k] & 0xff] + tab[256 + (v[k] & 0xff)], a.lo, a.hi);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    u[k] = add_one(a, u[k], v[k]);
+            }
             st16<YDT>(a.y, i0, u);
         } else {
             for (long long i = i0; i < i0 + 16 && i < a.count; ++i)

@@ -1880,6 +1880,16 @@ qnn_status make_add_args(qnn_dtype a_dtype, qnn_qparams a_q, qnn_dtype b_dtype, 
     // in [17, 40], nonzero multipliers)
     args.fast = rounding == QNN_ROUND_HALF_UP && args.ma > 0 && args.mb > 0 && args.na >= 17 && args.na <= 40 &&
                 args.nb >= 17 && args.nb <= 40;
+    // A term is round((v - zp) * m / 2^n) with |v - zp| at most that of the
+    // dtype's ends, within 2 of the real product: bound the sum of both
+    // terms and zp_y to decide whether int32 tables of the terms are exact.
+    auto term_bound = [](qnn_dtype dt, int32_t zp, int32_t m, int32_t n) {
+        const double lo = dt == QNN_INT8 ? -128.0 : 0.0, hi = dt == QNN_INT8 ? 127.0 : 255.0;
+        const double v = std::max(std::fabs(lo - zp), std::fabs(hi - zp));
+        return v * (double)m / std::ldexp(1.0, n) + 2.0;
+    };
+    args.tab_ok = term_bound(a_dtype, args.zpa, args.ma, args.na) + term_bound(b_dtype, args.zpb, args.mb, args.nb) +
+                      std::fabs((double)args.zp_y) < std::ldexp(1.0, 30);
     if (args.fast) {
         args.mah = args.ma >> 16;
         args.mal = args.ma & 0xffff;
@@ -1952,17 +1962,8 @@ qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams 
     qnn_status s = make_add_args((qnn_dtype)plan->y_dt, y_q, r_dtype, r_q, o_dtype, o_q, act, rounding, &args);
     if (s != QNN_OK)
         return s;
-    // Term tables (one term per operand byte): exact when every term, and
-    // so every sum, fits 32 bits.  A term is round((v - zp) * m / 2^n) with
-    // |v - zp| at most that of the dtype's ends, within 2 of the real product.
-    auto term_bound = [](qnn_dtype dt, int32_t zp, int32_t m, int32_t n) {
-        const double lo = dt == QNN_INT8 ? -128.0 : 0.0, hi = dt == QNN_INT8 ? 127.0 : 255.0;
-        const double v = std::max(std::fabs(lo - zp), std::fabs(hi - zp));
-        return v * (double)m / std::ldexp(1.0, n) + 2.0;
-    };
-    const double bound = term_bound((qnn_dtype)plan->y_dt, args.zpa, args.ma, args.na) +
-                         term_bound(r_dtype, args.zpb, args.mb, args.nb) + std::fabs((double)args.zp_y);
-    if (bound < std::ldexp(1.0, 30)) {
+    // term tables (one term per operand byte) where they are exact
+    if (args.tab_ok) {
         hipError_t e;
         if ((e = hipMalloc((void **)&plan->addtab, 512 * sizeof(int32_t))) != hipSuccess) {
             plan->addtab = nullptr;

@@ -111,6 +111,10 @@ struct AddArgs {
     // np = shift - 16, c = 2^(np - 1)); the operands are 8-bit, so the
     // zero-point-adjusted values fit 9 bits
     int32_t fast, mah, mal, npa, ca, mbh, mbl, npb, cb;
+    // tab_ok: every term, and so every sum of two terms plus zp_y, fits 32
+    // bits, so that the terms may be tabulated per operand byte as int32
+    // (the standalone kernel builds such tables in LDS per workgroup)
+    int32_t tab_ok;
     // fused residual add only: tab[b] = add_term_a of the byte b read as
     // the conv output's dtype, tab[256 + b] = add_term_b of the byte b read
     // as the residual's dtype, plus zp_y (512 int32 in device memory, built

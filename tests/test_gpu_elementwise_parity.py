@@ -102,11 +102,14 @@ def test_requantize_two_stage_ties(yt):
     assert differs > 1000
 
 
-@pytest.mark.parametrize("ratio", [2.0**13 * 1.5, 2.0**-10 * 1.5, 2.0**14 * 1.5, 2.0**-11 * 1.5, 0.62, 1.0])
+@pytest.mark.parametrize("ratio", [2.0**13 * 1.5, 2.0**-10 * 1.5, 2.0**14 * 1.5, 2.0**-11 * 1.5, 0.62, 1.0,
+                                   2.0**23 * 1.5])
 def test_add_shift_range(ratio):
     """Input / output scale ratios whose fixed-point shifts sit at the edges
     of the 24-bit product form of the add (shifts 17 and 40) and just
-    outside it (16 and 41: the 64-bit form), for every pair of input bytes."""
+    outside it (16 and 41: the 64-bit form), for every pair of input bytes;
+    the last ratio makes a term exceed 2^30, where the kernel adds without
+    its per-byte term tables."""
     a = np.repeat(np.arange(256, dtype=np.int32), 256).astype(np.uint8)
     b = np.tile(np.arange(256, dtype=np.int32), 256).astype(np.uint8)
     s_o = 0.01
