@@ -348,6 +348,7 @@ SHORT_SHAPES = [
     (W.ConvLayer("s", 8, 8, 64, 96, 1, 1, 1, (1, 1, 1, 1)), 2, dict(x_dtype="i8")),
     (W.ConvLayer("s", 6, 6, 192, 64, 1, 1), 3, {}),
     (W.ConvLayer("s", 10, 10, 128, 130, 1, 1), 2, dict(yt="i32")),
+    (W.ConvLayer("s", 28, 28, 64, 160, 1, 1), 4, {}),   # 75-150 tiles
 ]
 # K-steps each LDS-direct configuration holds in its short form (0: ring);
 # the last three are ring forms with two K-step groups per tile (the
