@@ -464,8 +464,6 @@ int oracle_add(const void *a, int32_t at, float s_a, int32_t zp_a,
     return 0;
 }
 
-/* Requantize of a single zero-point adjusted value v with real multiplier M
- * (exported for the exact-rational tests). */
 /* floor(a / b) for b > 0. */
 static int64_t floor_div(int64_t a, int64_t b)
 {
@@ -531,6 +529,8 @@ int oracle_pool2d(const void *x, int32_t xt, const int32_t *shape, const int32_t
     return bad ? -1 : 0;
 }
 
+/* Requantize of a single zero-point adjusted value v with real multiplier M
+ * (exported for the exact-rational tests). */
 int oracle_requantize_value(int64_t v, double M, int32_t zp_out, int32_t yt,
                             int64_t lo, int64_t hi, int32_t rounding, int64_t *out)
 {
