@@ -394,7 +394,10 @@ qnn_status qnn_time_next_kernel(void *start_event, void *stop_event);
  * multiples of 16 accept it;
  * others, int32 outputs and a second call return QNN_ERR_UNSUPPORTED and
  * leave the plan as it was.  r_ldc >= r_coff + K.  A fused plan runs only
- * through qnn_plan_run_residual.
+ * through qnn_plan_run_residual.  Where the add's per-byte terms fit 32-bit
+ * sums, the call tabulates them in a 2 KB device buffer that the plan owns
+ * (allocated here, one small kernel launched on the null stream and
+ * waited for); QNN_ERR_HIP if that fails.
  */
 qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams r_q, int32_t r_ldc,
                                  int32_t r_coff, qnn_dtype o_dtype, qnn_qparams o_q, qnn_clamp act,
