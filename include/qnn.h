@@ -397,7 +397,8 @@ qnn_status qnn_time_next_kernel(void *start_event, void *stop_event);
  * through qnn_plan_run_residual.  Where the add's per-byte terms fit 32-bit
  * sums, the call tabulates them in a 2 KB device buffer that the plan owns
  * (allocated here, one small kernel launched on the null stream and
- * waited for); QNN_ERR_HIP if that fails.
+ * waited for); QNN_ERR_ALLOC or QNN_ERR_HIP if that fails, the plan as it
+ * was.
  */
 qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams r_q, int32_t r_ldc,
                                  int32_t r_coff, qnn_dtype o_dtype, qnn_qparams o_q, qnn_clamp act,

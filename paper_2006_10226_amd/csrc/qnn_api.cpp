@@ -1967,7 +1967,7 @@ qnn_status qnn_plan_set_residual(qnn_plan *plan, qnn_dtype r_dtype, qnn_qparams 
         hipError_t e;
         if ((e = hipMalloc((void **)&plan->addtab, 512 * sizeof(int32_t))) != hipSuccess) {
             plan->addtab = nullptr;
-            return hip_fail(e, "plan_set_residual: table allocation");
+            return fail(QNN_ERR_ALLOC, "plan_set_residual: table allocation: %s", hipGetErrorString(e));
         }
         if ((e = launch_add_table(args, plan->y_dt == QNN_INT8 ? 1 : 0, r_dtype == QNN_INT8 ? 1 : 0, plan->addtab,
                                   nullptr)) != hipSuccess ||
