@@ -145,3 +145,67 @@ def test_fused_add_refused():
         with pytest.raises(Q.QnnError, match="UNSUPPORTED"):
             p.set_residual("u8", 0.02, 10, 0.03, 5, "u8")
         p.close()
+
+
+# LDS-direct and tap-walk configurations with a fused-add instantiation
+# (waves of at most 64 x 64 outputs) and those without one.
+DMA_FUSED = [t for t in range(29) if t not in (8, 9, 10, 11)]
+DMA_SHORT = {t: s for t, s in zip(range(15, 26), [1, 1, 1, 1, 2, 2, 2, 2, 4, 4, 4])}
+TAP_FUSED = list(range(8))
+
+
+def _fused_case(layer, N, seed, env_kw, what, **kw):
+    c = W.conv_case(layer, N, seed=seed, **kw)
+    mid = run_oracle(c)
+    full, r = _residual(mid.shape, "i8", seed=seed + 1)
+    ref = O.add(mid, c.s_y, c.zp_y, r, 0.041, -9, 0.05, 3 if c.yt == "i8" else 110, c.yt, None)
+    y_ldc = -(-layer.Cout // 16) * 16
+    with env(**env_kw):
+        p, keep = make_plan(c, y_ldc=y_ldc)
+    d = p.describe()
+    p.set_residual("i8", 0.041, -9, 0.05, 3 if c.yt == "i8" else 110, c.yt)
+    with env(**env_kw):
+        y = p.run(dev(c.x), residual=dev(full))
+    torch.cuda.synchronize()
+    p.close()
+    log(f"fused {what}: {d}")
+    assert_equal(y.cpu().numpy()[..., :layer.Cout], ref, f"fused {what}: {d}")
+    return d
+
+
+@pytest.mark.parametrize("tile", DMA_FUSED)
+def test_fused_add_every_dma_tile(tile):
+    """Every LDS-direct configuration that has the fused epilogue: a 1x1
+    conv within its short form's K-steps (or a 3x3 conv with padding,
+    int8 input and weight zero points for the ring forms), ragged channels
+    and pixels."""
+    if tile in DMA_SHORT:
+        layer = W.ConvLayer("f1", 9, 11, 64 * DMA_SHORT[tile], 88, 1, 1)
+        kw = {}
+    else:
+        layer = W.ConvLayer("f3", 10, 9, 64, 136, 3, 3, 1, (1, 1, 1, 1))
+        kw = dict(x_dtype="i8", zp_w="channel", yt="i8")
+    d = _fused_case(layer, 3, 500 + tile, dict(QNN_DMA=tile), f"dma {tile}", **kw)
+    assert d.startswith("conv_dma"), d
+
+
+@pytest.mark.parametrize("tile", TAP_FUSED)
+def test_fused_add_every_tap_tile(tile):
+    layer = W.ConvLayer("t3", 11, 10, 128, 100, 3, 3, 1, (1, 1, 1, 1))
+    d = _fused_case(layer, 2, 600 + tile, dict(QNN_TAP=tile), f"tap {tile}", yt="i8")
+    assert d.startswith("conv_tap"), d
+
+
+@pytest.mark.parametrize("fam,tile", [("QNN_DMA", 8), ("QNN_DMA", 9), ("QNN_DMA", 10), ("QNN_DMA", 11),
+                                      ("QNN_TAP", 8), ("QNN_TAP", 9), ("QNN_TAP", 10), ("QNN_TAP", 11)])
+def test_fused_add_refused_for_large_wave_tiles(fam, tile):
+    """Configurations whose waves hold more than 64 x 64 outputs have no
+    fused epilogue: the plan refuses the add and runs as before."""
+    layer = W.ConvLayer("b", 8, 8, 128, 128, 1, 1)
+    c = W.conv_case(layer, 4, seed=tile)
+    with env(**{fam: tile}):
+        p, keep = make_plan(c)
+    with pytest.raises(Q.QnnError, match="UNSUPPORTED"):
+        p.set_residual("u8", 0.02, 10, 0.03, 5, "u8")
+    assert_equal(p.run(dev(c.x)).cpu().numpy(), run_oracle(c), f"{fam}={tile} refused plan still runs")
+    p.close()
