@@ -70,9 +70,9 @@ __device__ __forceinline__ uint32_t requant4(const ConvArgs &a, v4i acc, const v
 // (residual_prefetch), so that their memory latency overlaps the
 // requantize and the staging.
 
-// Residual bytes of one chunk (n <= 16 channels from k0 at pixel m): a
-// 16-byte load where rows are 16-byte aligned and the chunk is whole,
-// else byte loads (then `vec` is false and the caller loads later).
+// Whether the residual bytes of a chunk of n <= 16 channels come by one
+// 16-byte load (residual rows 16-byte aligned, chunk whole); the copy-out
+// loads the others byte by byte.
 __device__ __forceinline__ bool residual_chunk_vec(const ConvArgs &a, int n)
 {
     return a.res_vec && n == 16;
@@ -96,10 +96,10 @@ __device__ __forceinline__ void residual_prefetch(const ConvArgs &a, int c0, int
     }
 }
 
-// The add of 16 requantized output bytes v (channels k0 .. k0 + n - 1 of
-// pixel m, dtype ydt) and their residual bytes r (rdt); the sum's bytes
-// replace the outputs.  One 4-byte word per pass, the words rotated through
-// position 0 (a rolled loop keeps a single copy of add_one's code).
+// The add of 16 requantized output bytes v (dtype ydt) and the residual
+// bytes r of the same elements (rdt), through the add's own arithmetic;
+// returns the sum's bytes.  One 4-byte word per pass, the words rotated
+// through position 0 (a rolled loop keeps a single copy of add_one's code).
 __device__ __forceinline__ v4i residual_add16(const ConvArgs &a, v4i v, v4i r)
 {
     v4i o = v4i{0, 0, 0, 0};
