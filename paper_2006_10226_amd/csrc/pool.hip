@@ -45,7 +45,12 @@ __device__ __forceinline__ void pool_load(const int8_t *p, unsigned (&w)[(V + 3)
 // each loaded word are summed in the two 16-bit halves of one register,
 // bytes 1 and 3 in another (int8 biased by +128 first); 257 * 255 < 2^16,
 // so no half carries into the other.
-template <bool SIGNED, bool MAX, int V, bool PACK = false>
+// W3 (3x3 windows): the nine cells are loaded before any is used, so their
+// memory latencies overlap (the loops of the general form wait once per
+// window row, which is what small, latency-bound launches pay for); a cell
+// outside the input reads the window's first cell inside it instead and
+// is left out of the sum or maximum.
+template <bool SIGNED, bool MAX, int V, bool PACK = false, bool W3 = false>
 __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
 {
     constexpr int NW = (V + 3) / 4;
@@ -72,6 +77,40 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
 #pragma unroll
         for (int k = 0; k < NW; ++k)
             even[k] = odd[k] = 0;
+        auto take = [&](const unsigned (&w)[NW]) {
+            if constexpr (PACK) {
+#pragma unroll
+                for (int k = 0; k < NW; ++k) {
+                    const unsigned x = SIGNED ? w[k] ^ 0x80808080u : w[k];
+                    even[k] += x & 0x00ff00ffu;
+                    odd[k] += (x >> 8) & 0x00ff00ffu;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < V; ++i) {
+                    const unsigned b = (w[i / 4] >> (8 * (i % 4))) & 0xffu;
+                    const int v = SIGNED ? (int)(signed char)b : (int)b;
+                    acc[i] = MAX ? max(acc[i], v) : acc[i] + v;
+                }
+            }
+        };
+        if constexpr (W3) {
+            if (r0 < r1 && s0 < s1) {
+                unsigned w9[9][NW];
+#pragma unroll
+                for (int t = 0; t < 9; ++t) {
+                    const int r = t / 3, c = t % 3;
+                    const bool in = r >= r0 && r < r1 && c >= s0 && c < s1;
+                    pool_load<V>(base + ((size_t)(h0 + (in ? r : r0)) * a.W + (w0 + (in ? c : s0))) * a.C, w9[t]);
+                }
+#pragma unroll
+                for (int t = 0; t < 9; ++t) {
+                    const int r = t / 3, c = t % 3;
+                    if (r >= r0 && r < r1 && c >= s0 && c < s1)
+                        take(w9[t]);
+                }
+            }
+        } else {
         for (int r = r0; r < r1; ++r) {
             const int8_t *row = base + ((size_t)(h0 + r) * a.W + (w0 + s0)) * a.C;
             // unrolled so that several cells' loads are in flight at once
@@ -79,22 +118,9 @@ __global__ void __launch_bounds__(256) pool_kernel(PoolArgs a)
             for (int s = s0; s < s1; ++s, row += a.C) {
                 unsigned w[NW];
                 pool_load<V>(row, w);
-                if constexpr (PACK) {
-#pragma unroll
-                    for (int k = 0; k < NW; ++k) {
-                        const unsigned x = SIGNED ? w[k] ^ 0x80808080u : w[k];
-                        even[k] += x & 0x00ff00ffu;
-                        odd[k] += (x >> 8) & 0x00ff00ffu;
-                    }
-                } else {
-#pragma unroll
-                    for (int i = 0; i < V; ++i) {
-                        const unsigned b = (w[i / 4] >> (8 * (i % 4))) & 0xffu;
-                        const int v = SIGNED ? (int)(signed char)b : (int)b;
-                        acc[i] = MAX ? max(acc[i], v) : acc[i] + v;
-                    }
-                }
+                take(w);
             }
+        }
         }
         if constexpr (PACK) {
             const int bias = SIGNED ? 128 * (r1 - r0) * (s1 - s0) : 0;
@@ -253,15 +279,24 @@ hipError_t launch_pool_split(const PoolArgs &a, bool is_signed, int vec, hipStre
     return hipGetLastError();
 }
 
+template <bool SIGNED, bool MAX, bool W3>
+static void launch_pool_w(const PoolArgs &a, int vec, dim3 grid, hipStream_t s)
+{
+    const bool pack = !MAX && (long long)a.R * a.S <= 257;
+    if (vec == 16 && pack) launch_main((pool_kernel<SIGNED, MAX, 16, !MAX, W3>), grid, dim3(256), 0, s, a);
+    else if (vec == 16) launch_main((pool_kernel<SIGNED, MAX, 16, false, W3>), grid, dim3(256), 0, s, a);
+    else if (vec == 4 && pack) launch_main((pool_kernel<SIGNED, MAX, 4, !MAX, W3>), grid, dim3(256), 0, s, a);
+    else if (vec == 4) launch_main((pool_kernel<SIGNED, MAX, 4, false, W3>), grid, dim3(256), 0, s, a);
+    else launch_main((pool_kernel<SIGNED, MAX, 1, false, W3>), grid, dim3(256), 0, s, a);
+}
+
 template <bool SIGNED, bool MAX>
 static void launch_pool_t(const PoolArgs &a, int vec, dim3 grid, hipStream_t s)
 {
-    const bool pack = !MAX && (long long)a.R * a.S <= 257;
-    if (vec == 16 && pack) launch_main((pool_kernel<SIGNED, MAX, 16, !MAX>), grid, dim3(256), 0, s, a);
-    else if (vec == 16) launch_main((pool_kernel<SIGNED, MAX, 16>), grid, dim3(256), 0, s, a);
-    else if (vec == 4 && pack) launch_main((pool_kernel<SIGNED, MAX, 4, !MAX>), grid, dim3(256), 0, s, a);
-    else if (vec == 4) launch_main((pool_kernel<SIGNED, MAX, 4>), grid, dim3(256), 0, s, a);
-    else launch_main((pool_kernel<SIGNED, MAX, 1>), grid, dim3(256), 0, s, a);
+    if (a.R == 3 && a.S == 3)
+        launch_pool_w<SIGNED, MAX, true>(a, vec, grid, s);
+    else
+        launch_pool_w<SIGNED, MAX, false>(a, vec, grid, s);
 }
 
 hipError_t launch_pool(const PoolArgs &a, bool is_signed, int vec, hipStream_t s)
