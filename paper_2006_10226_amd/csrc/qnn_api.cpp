@@ -1994,6 +1994,8 @@ qnn_status qnn_plan_run_residual(const qnn_plan *plan, void *stream, const void 
         return fail(QNN_ERR_NULL, "plan_run_residual: plan is NULL");
     if (!plan->fused)
         return fail(QNN_ERR_UNSUPPORTED, "plan_run_residual: the plan adds no residual (qnn_plan_set_residual)");
+    if (plan->conv.M == 0)
+        return QNN_OK;   // empty batch: nothing to read or write, as in qnn_plan_run
     if (!residual)
         return fail(QNN_ERR_NULL, "plan_run_residual: residual is NULL");
     return run_plan(plan, (hipStream_t)stream, x, y, workspace, residual);

@@ -257,6 +257,14 @@ def test_empty_batch_is_noop():
     p.run(x)
     torch.cuda.synchronize()
     p.close()
+    # a fused residual add on an empty batch: nothing to read or write either
+    with env(QNN_DMA=0):
+        p, keep = make_plan(c, N=0)
+    p.set_residual("u8", 0.02, 10, 0.03, 5, "u8")
+    y = p.run(x, residual=torch.empty((0, 14, 14, 64), dtype=torch.uint8, device="cuda"))
+    torch.cuda.synchronize()
+    assert y.shape == (0, 14, 14, 64)
+    p.close()
 
 
 def test_plan_workspace_and_streams():
