@@ -446,6 +446,10 @@ DW3_SHAPES = [
     (W.ConvLayer("d", 10, 38, 32, 32, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, {}),
     (W.ConvLayer("d", 15, 33, 48, 48, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2, dict(zp_w="channel")),
     (W.ConvLayer("d", 9, 20, 16, 16, 3, 3, 1, (0, 2, 1, 0), depthwise=True), 3, dict(x_dtype="i8")),
+    # wider channel counts: 128 and 192 channels, stride 1 and 2
+    (W.ConvLayer("d", 10, 12, 128, 128, 3, 3, 1, (1, 1, 1, 1), depthwise=True), 2, {}),
+    (W.ConvLayer("d", 13, 14, 192, 192, 3, 3, 2, (1, 1, 1, 1), depthwise=True), 2,
+     dict(x_dtype="i8", zp_w="channel")),
 ]
 
 
